@@ -1,0 +1,189 @@
+/*
+ * occam.h -- C ABI of the MI355X (gfx950) register-anchored relative evidence
+ * test of OccamToken (arXiv 2605.29657): the data-parallel step that decides
+ * which visual tokens reach an LLM's prefill.
+ *
+ * The paper's rule (Sec. 3.2, Eq. framework; Sec. 3.4 Eq. stage1; Sec. 3.5
+ * Eq. stage2) keeps a visual token v of sample x when
+ *
+ *      s_x(v) >= lambda * s_x(r(x)),
+ *
+ * where s_x is the head-averaged softmax attention that the anchor rows pay to
+ * each key and r(x) is the test-time register token.  One entry point exists
+ * per step of that rule, plus a fused one:
+ *
+ *   occam_score      steps 1-2: anchor logits, row softmax, head mean, anchor
+ *                    reduction (Eq. (1); Eq. EQ:CLS; Eq. text_scoring)
+ *   occam_threshold  step 3: tau_b = lambda * s_b(r) (Eqs.
+ *                    stage1_threshold_appendix, stage2_set_appendix)
+ *   occam_select     step 4-5: s(v) >= tau test and ascending prefix-scan
+ *                    compaction of the survivors (Eqs. stage1, stage2)
+ *   occam_gather     step 5: dense copy of the survivors' rows (the pruned
+ *                    sequence [S; T] of Algorithm 1)
+ *   occam_prune      all of the above on one stream, no host synchronisation
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Shapes.  B samples; H query heads, Hkv key heads (H % Hkv == 0; query head h
+ * reads key head h / (H / Hkv)); head dim d; R register keys; T_b anchor rows
+ * of sample b (T = 1: the vision encoder's CLS row, Stage I; T > 1: the LLM's
+ * text rows, Stage II); N_b visual candidates of sample b.
+ *
+ * Layouts (row-major, token-major, packed over the batch):
+ *   q        [(qo_b + t) * H * d + h * d + e]        anchor rows
+ *   k        [(ko_b + s) * Hkv * d + g * d + e]      s in [0,R): registers,
+ *                                                   s in [R, R+N_b): visual
+ *   scores   [ko_b + s]                              float32
+ *   row_lse  [(qo_b + t) * H + h]                    float32, natural log
+ *   tau      [b]                                     float32
+ * with qo_b = q_offsets[b] (or b * rows) and ko_b = key_offsets[b] (or
+ * b * (R + cands)).  The candidate prefix co_b = ko_b - R * b counts the
+ * visual tokens of the samples before b.
+ *
+ * Survivor lists are packed over the batch: sample b's survivors occupy
+ * kept_idx[kept_offsets[b] .. kept_offsets[b] + kept_count[b]), ascending
+ * candidate-local indices v in [0, N_b).  Registers are never candidates and
+ * are never listed; the caller keeps them (the paper's "union {r}").
+ *
+ * Ownership.  Every pointer argument is DEVICE memory owned by the caller,
+ * except `const occam_problem *` and `const occam_rows *`, which are host
+ * structs read during the call only.  The library allocates no memory and
+ * keeps no mutable global state; calls on different streams may overlap when
+ * their output and workspace buffers are distinct.
+ *
+ * Errors.  Arguments are validated on the host before anything is enqueued;
+ * on any error nothing is launched and the outputs are untouched.  Calls are
+ * asynchronous: kernel faults surface at the caller's next synchronisation of
+ * `stream`.  Inputs must be finite.  Device-side offsets must be
+ * non-decreasing with 1 <= T_b <= max_rows and 0 <= N_b <= max_cands.
+ *
+ * Precision.  Logits and probabilities are computed in float32 from float32
+ * or bfloat16 inputs; bfloat16 products are exact in float32.
+ */
+#ifndef OCCAM_H
+#define OCCAM_H
+
+#include <stddef.h>
+#include <stdint.h>
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define OCCAM_VERSION 1
+#define OCCAM_MAX_ROW_TENSORS 8
+
+typedef enum {
+    OCCAM_OK = 0,
+    OCCAM_ERR_INVALID_ARG = 1, /* a null/misaligned pointer or an impossible shape   */
+    OCCAM_ERR_UNSUPPORTED = 2, /* a valid shape this build has no kernel for         */
+    OCCAM_ERR_WORKSPACE = 3,   /* ws_bytes < occam_workspace_size(problem)          */
+    OCCAM_ERR_HIP = 4          /* a kernel launch was rejected by the HIP runtime    */
+} occam_status;
+
+typedef enum { OCCAM_F32 = 0, OCCAM_BF16 = 1 } occam_dtype;
+
+/* How the R register scores are combined into s(r).  The paper builds one
+ * register (Appendix, "Parameter settings"); with several, MEAN is the default
+ * reading and equals the paper's rule at R = 1. */
+typedef enum { OCCAM_REG_MEAN = 0, OCCAM_REG_MAX = 1, OCCAM_REG_SUM = 2 } occam_reg_reduce;
+
+typedef struct {
+    int32_t batch;          /* B >= 1                                                */
+    int32_t num_heads;      /* H >= 1                                                */
+    int32_t num_kv_heads;   /* Hkv >= 1, H % Hkv == 0                                */
+    int32_t head_dim;       /* d: multiple of 8 (bf16) or 4 (f32), <= 256            */
+    int32_t num_registers;  /* R in [1, 32]                                          */
+    int32_t rows;           /* T when q_offsets == NULL (>= 1)                       */
+    int32_t cands;          /* N when key_offsets == NULL (>= 0)                     */
+    const int32_t *q_offsets;   /* device [B+1] prefix of T_b, or NULL (uniform)     */
+    const int32_t *key_offsets; /* device [B+1] prefix of R + N_b, or NULL (uniform) */
+    int32_t max_rows;       /* upper bound of T_b when q_offsets != NULL             */
+    int32_t max_cands;      /* upper bound of N_b when key_offsets != NULL           */
+    int32_t dtype;          /* occam_dtype of q and k                                */
+    float softmax_scale;    /* 0 => 1/sqrt(d), the scale of Eq. (1)                  */
+} occam_problem;
+
+/* One row tensor gathered with the survivors (occam_gather / occam_prune).
+ * The source row of visual token v of sample b is
+ *     co_b + b * src_pad_rows + src_row0 + v
+ * i.e. each sample owns N_b + src_pad_rows consecutive rows, of which the
+ * visual ones start at src_row0 (a hidden-state tensor of visual tokens only:
+ * pad 0, row0 0; the key/value rows of [registers ; visual]: pad R, row0 R).
+ * The destination row of survivor i of sample b is kept_offsets[b] + i.
+ * src/dst and both strides must be multiples of 4 bytes, row_bytes of 4;
+ * 16-byte multiples take the vector path. */
+typedef struct {
+    const void *src;
+    void *dst;
+    int64_t src_pad_rows;
+    int64_t src_row0;
+    int64_t src_row_stride_bytes;
+    int64_t dst_row_stride_bytes;
+    int64_t row_bytes;
+} occam_rows;
+
+/* Human-readable name of a status code (static storage). */
+const char *occam_status_string(occam_status status);
+
+/* OCCAM_VERSION of the built library. */
+int32_t occam_version(void);
+
+/* Bytes of device workspace that every call below may use for this problem
+ * (0 for an invalid problem).  The workspace needs no initialisation and
+ * holds nothing between calls. */
+size_t occam_workspace_size(const occam_problem *problem);
+
+/* Steps 1-2 (Eq. (1); Eq. EQ:CLS; Eq. text_scoring).  For every sample, every
+ * anchor row t and head h, the softmax over the R + N_b keys of
+ * scale * <q[t,h], k[s, h/(H/Hkv)]> is averaged over heads; the score of a
+ * visual key is the max of that average over the T_b rows, the score of a
+ * register the mean over the rows (T_b = 1: the CLS row itself).
+ * row_lse (nullable): the natural-log softmax normaliser of each (row, head)
+ * over a larger key set (e.g. the LLM's full causal prefix); when given,
+ * probabilities are exp(logit - row_lse) instead of the softmax over the keys
+ * given.  Writes scores[sum_b (R + N_b)]. */
+occam_status occam_score(const occam_problem *problem, const void *q, const void *k,
+                         const float *row_lse, float *scores,
+                         void *workspace, size_t ws_bytes, hipStream_t stream);
+
+/* Step 3 (Eqs. stage1_threshold_appendix, stage2_set_appendix):
+ * tau[b] = lambda * reduce(scores[ko_b + 0 .. ko_b + R)), lambda finite >= 0. */
+occam_status occam_threshold(const occam_problem *problem, const float *scores,
+                             float lambda, int32_t reduce, float *tau, hipStream_t stream);
+
+/* Steps 4-5 (Eq. stage1 / Eq. stage2): keep visual token v of sample b iff
+ * scores[ko_b + R + v] >= tau[b]; write the survivors ascending and packed,
+ * kept_count[B] and kept_offsets[B+1] (exclusive prefix of the counts).
+ * index_map (nullable, [sum N_b]): write index_map[co_b + v] instead of v,
+ * which chains Stage II onto Stage I's original token indices.
+ * kept_idx must hold sum_b N_b entries (the worst case). */
+occam_status occam_select(const occam_problem *problem, const float *scores, const float *tau,
+                          const int32_t *index_map, int32_t *kept_idx, int32_t *kept_count,
+                          int32_t *kept_offsets, void *workspace, size_t ws_bytes,
+                          hipStream_t stream);
+
+/* Step 5, materialisation (Algorithm 1, the pruned sequence): for each of
+ * the n row tensors, copy the row of every listed survivor, byte for byte, to
+ * the packed destination.  kept_idx values are read as candidate-local v. */
+occam_status occam_gather(const occam_problem *problem, int32_t n, const occam_rows *tensors,
+                          const int32_t *kept_idx, const int32_t *kept_offsets,
+                          hipStream_t stream);
+
+/* Steps 1-5 fused on `stream` without host synchronisation: scores, tau,
+ * survivors and the gather of n row tensors (n may be 0).  scores may be NULL
+ * (kept in the workspace).  With index_map the emitted kept_idx values are
+ * remapped as in occam_select while the gather still reads local rows v. */
+occam_status occam_prune(const occam_problem *problem, const void *q, const void *k,
+                         const float *row_lse, float lambda, int32_t reduce,
+                         const int32_t *index_map, int32_t n, const occam_rows *tensors,
+                         float *scores, float *tau, int32_t *kept_idx, int32_t *kept_count,
+                         int32_t *kept_offsets, void *workspace, size_t ws_bytes,
+                         hipStream_t stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* OCCAM_H */

@@ -1,0 +1,262 @@
+/*
+ * occam_oracle.c -- plain fp64 CPU oracle for OccamToken's register-anchored
+ * relative evidence test (arXiv 2605.29657).
+ *
+ * TEST INFRASTRUCTURE ONLY.  This file is the reference that the HIP path is
+ * checked against.  Only the tests, the smoke check and the benchmark's CPU
+ * baseline leg may load it.  It shares no code, header, table or helper with
+ * the GPU library, and the GPU library never calls it.
+ *
+ * Everything is computed in double precision with straightforward loops, in
+ * the order the paper states the method:
+ *
+ *   1. attention logits of each anchor row against [registers ; visual] keys,
+ *      scaled by 1/sqrt(d_h)                       (Sec. 3.1, Eq. (1))
+ *   2. row softmax, then the mean over attention heads
+ *                                                  (Eq. (1); Appendix "Stage-I
+ *                                                   pruning": the vision map is
+ *                                                   averaged over heads)
+ *   3. anchor-row reduction: a single CLS row is taken as is (Eq. EQ:CLS);
+ *      text rows are reduced by max for visual tokens and by mean for the
+ *      register                                    (Eq. text_scoring)
+ *   4. threshold tau = lambda * s(r)               (Eqs. stage1_threshold_appendix,
+ *                                                   stage2_set_appendix)
+ *   5. keep visual tokens with s(v) >= tau; the register is never a candidate
+ *                                                  (Eqs. stage1, stage2, framework)
+ *   6. ascending list of survivors per sample, packed over the batch, and a
+ *      byte copy of their rows (the pruned sequence [S; T] of Algorithm 1)
+ *
+ * Readings where the paper is silent (all listed in the design notes):
+ *   - several registers: s(r) is the mean over the R register scores (MAX and
+ *     SUM are offered as alternatives);
+ *   - Stage II heads: the head mean is taken before the max/mean over text rows;
+ *   - the softmax runs over the R+N keys given, unless the caller supplies the
+ *     per-(row, head) log-sum-exp of a larger key set;
+ *   - grouped-query attention: query head h reads key head h / (H / Hkv).
+ *
+ * Layouts (token-major, packed over a ragged batch):
+ *   q[(q_off[b] + t) * H * d + h * d + e]          anchor rows of sample b
+ *   k[(k_off[b] + s) * Hkv * d + g * d + e]        s in [0,R) registers,
+ *                                                  s in [R, R+N_b) visual
+ *   scores[k_off[b] + s]
+ *   candidate prefix co_b = k_off[b] - R * b (visual tokens before sample b)
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define ORACLE_F32 0
+#define ORACLE_BF16 1
+
+#define ORACLE_REG_MEAN 0
+#define ORACLE_REG_MAX 1
+#define ORACLE_REG_SUM 2
+
+/* bfloat16 is the upper half of an IEEE binary32; widening is exact. */
+static double bf16_to_double(uint16_t bits)
+{
+    uint32_t w = ((uint32_t)bits) << 16;
+    float f;
+    memcpy(&f, &w, sizeof f);
+    return (double)f;
+}
+
+static double load_elem(const void *base, int dtype, int64_t i)
+{
+    if (dtype == ORACLE_BF16)
+        return bf16_to_double(((const uint16_t *)base)[i]);
+    return (double)((const float *)base)[i];
+}
+
+/* Exposed so a test can compare the decoder with an independent one. */
+double oracle_bf16_to_double(uint16_t bits) { return bf16_to_double(bits); }
+
+/*
+ * Steps 1-3: scores of every key of every sample.
+ * scale     : softmax temperature; the paper's value is 1/sqrt(d).
+ * row_lse   : optional natural-log normaliser per (anchor row, head),
+ *             laid out [(q_off[b] + t) * H + h]; NULL = softmax over the keys
+ *             given.
+ * Returns 0, or -1 on a shape error.
+ */
+int oracle_scores(int B, int H, int Hkv, int d, int R,
+                  const int64_t *q_off, const int64_t *k_off,
+                  int dtype, const void *q, const void *k,
+                  double scale, const double *row_lse, double *scores)
+{
+    if (B < 0 || H < 1 || Hkv < 1 || H % Hkv != 0 || d < 1 || R < 1)
+        return -1;
+    for (int b = 0; b < B; ++b)
+        if (q_off[b + 1] - q_off[b] < 1 || k_off[b + 1] - k_off[b] < R)
+            return -1;
+
+    const int group = H / Hkv;
+    int err = 0;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int b = 0; b < B; ++b) {
+        const int64_t T = q_off[b + 1] - q_off[b];
+        const int64_t S = k_off[b + 1] - k_off[b];
+        double *logit = (double *)malloc(sizeof(double) * (size_t)S);
+        double *abar = (double *)calloc((size_t)(T * S), sizeof(double));
+        double *qrow = (double *)malloc(sizeof(double) * (size_t)d);
+        if (!logit || !abar || !qrow) {
+#pragma omp atomic write
+            err = 1;
+            free(logit); free(abar); free(qrow);
+            continue;
+        }
+        for (int h = 0; h < H; ++h) {
+            const int g = h / group; /* key head read by query head h */
+            for (int64_t t = 0; t < T; ++t) {
+                const int64_t qrow_idx = q_off[b] + t;
+                for (int e = 0; e < d; ++e)
+                    qrow[e] = load_elem(q, dtype, (qrow_idx * H + h) * d + e);
+                /* Step 1: l_s = scale * <q_t, k_s> (Eq. (1)). */
+                for (int64_t s = 0; s < S; ++s) {
+                    const int64_t krow = k_off[b] + s;
+                    double dot = 0.0;
+                    for (int e = 0; e < d; ++e)
+                        dot += qrow[e] * load_elem(k, dtype, (krow * Hkv + g) * d + e);
+                    logit[s] = scale * dot;
+                }
+                /* Step 2: A_s = softmax(l)_s over the S keys (Eq. (1)), or
+                 * exp(l_s - lse) with a caller-supplied normaliser. */
+                double *arow = abar + t * S;
+                if (row_lse) {
+                    const double lse = row_lse[qrow_idx * H + h];
+                    for (int64_t s = 0; s < S; ++s)
+                        arow[s] += exp(logit[s] - lse) / (double)H;
+                } else {
+                    double m = logit[0];
+                    for (int64_t s = 1; s < S; ++s)
+                        if (logit[s] > m) m = logit[s];
+                    double z = 0.0;
+                    for (int64_t s = 0; s < S; ++s)
+                        z += exp(logit[s] - m);
+                    /* head mean: accumulate A / H */
+                    for (int64_t s = 0; s < S; ++s)
+                        arow[s] += (exp(logit[s] - m) / z) / (double)H;
+                }
+            }
+        }
+        /* Step 3: visual score = max over anchor rows of the head-mean map;
+         * register score = mean over anchor rows (Eq. text_scoring).  With one
+         * anchor row both are the CLS row itself (Eq. EQ:CLS). */
+        double *out = scores + k_off[b];
+        for (int64_t s = 0; s < S; ++s) {
+            if (s < R) {
+                double acc = 0.0;
+                for (int64_t t = 0; t < T; ++t)
+                    acc += abar[t * S + s];
+                out[s] = acc / (double)T;
+            } else {
+                double mx = abar[s];
+                for (int64_t t = 1; t < T; ++t)
+                    if (abar[t * S + s] > mx) mx = abar[t * S + s];
+                out[s] = mx;
+            }
+        }
+        free(logit);
+        free(abar);
+        free(qrow);
+    }
+    return err ? -1 : 0;
+}
+
+/*
+ * Step 4: tau_b = lambda * s_b(r), with s_b(r) the mean (or max, or sum) of
+ * the R register scores of sample b.
+ */
+int oracle_threshold(int B, int R, const int64_t *k_off, const double *scores,
+                     double lambda, int reduce, double *tau)
+{
+    if (B < 0 || R < 1 || !(lambda >= 0.0) || isinf(lambda))
+        return -1;
+    if (reduce != ORACLE_REG_MEAN && reduce != ORACLE_REG_MAX && reduce != ORACLE_REG_SUM)
+        return -1;
+    for (int b = 0; b < B; ++b) {
+        const double *reg = scores + k_off[b];
+        double sr;
+        if (reduce == ORACLE_REG_MAX) {
+            sr = reg[0];
+            for (int r = 1; r < R; ++r)
+                if (reg[r] > sr) sr = reg[r];
+        } else {
+            sr = 0.0;
+            for (int r = 0; r < R; ++r)
+                sr += reg[r];
+            if (reduce == ORACLE_REG_MEAN)
+                sr /= (double)R;
+        }
+        tau[b] = lambda * sr;
+    }
+    return 0;
+}
+
+/*
+ * Step 5: keep visual token v of sample b iff scores[k_off[b] + R + v] >= tau[b].
+ * kept_idx is packed over the batch: sample b's survivors, ascending, occupy
+ * kept_idx[kept_offsets[b] .. kept_offsets[b] + kept_count[b]).  With an
+ * index_map the value written is index_map[co_b + v] instead of v.
+ */
+int oracle_select(int B, int R, const int64_t *k_off, const double *scores,
+                  const double *tau, const int32_t *index_map,
+                  int32_t *kept_idx, int32_t *kept_count, int32_t *kept_offsets)
+{
+    if (B < 0 || R < 1)
+        return -1;
+    int32_t pos = 0;
+    kept_offsets[0] = 0;
+    for (int b = 0; b < B; ++b) {
+        const int64_t N = k_off[b + 1] - k_off[b] - R;
+        const int64_t co = k_off[b] - (int64_t)R * b;
+        int32_t cnt = 0;
+        for (int64_t v = 0; v < N; ++v) {
+            if (scores[k_off[b] + R + v] >= tau[b]) {
+                kept_idx[pos + cnt] = index_map ? index_map[co + v] : (int32_t)v;
+                ++cnt;
+            }
+        }
+        kept_count[b] = cnt;
+        pos += cnt;
+        kept_offsets[b + 1] = pos;
+    }
+    return 0;
+}
+
+/*
+ * Step 6: dst row kept_offsets[b] + i  <-  src row of (b, kept_idx[...]).
+ * Each sample owns N_b + src_pad_rows consecutive source rows whose visual
+ * rows start at src_row0, so the source row of visual token v of sample b is
+ * co_b + b * src_pad_rows + src_row0 + v.  Rows are copied byte for byte.
+ */
+int oracle_gather(int B, int R, const int64_t *k_off,
+                  const unsigned char *src, int64_t src_pad_rows,
+                  int64_t src_row0, int64_t src_row_stride_bytes,
+                  unsigned char *dst, int64_t dst_row_stride_bytes, int64_t row_bytes,
+                  const int32_t *kept_idx, const int32_t *kept_offsets)
+{
+    if (B < 0 || R < 1 || row_bytes < 0)
+        return -1;
+    for (int b = 0; b < B; ++b) {
+        const int64_t co = k_off[b] - (int64_t)R * b;
+        const int64_t base = co + (int64_t)b * src_pad_rows + src_row0;
+        for (int32_t i = kept_offsets[b]; i < kept_offsets[b + 1]; ++i) {
+            const int64_t row = base + kept_idx[i];
+            memcpy(dst + (int64_t)i * dst_row_stride_bytes,
+                   src + row * src_row_stride_bytes, (size_t)row_bytes);
+        }
+    }
+    return 0;
+}
+
+/* Effective number of attended tokens, exp(-sum a ln a) (Sec. 3.2, Obs. 1). */
+double oracle_neff(const double *alpha, int64_t n)
+{
+    double h = 0.0;
+    for (int64_t i = 0; i < n; ++i)
+        if (alpha[i] > 0.0)
+            h -= alpha[i] * log(alpha[i]);
+    return exp(h);
+}
