@@ -1,0 +1,231 @@
+"""Throughput of the fused register-anchored prune on one MI355X.
+
+One step = the whole pruning path over one batch of the LLaVA-NeXT-shaped workload
+(B=32 images, 2880 visual tokens + 4 registers each, bfloat16):
+  Stage I   occam_prune with the CLS row (H=16, d=64): scores, tau, survivors, and
+            the gather of the survivors' 1024-wide vision hidden rows;
+  Stage II  occam_prune with 128 text rows (H=32, d=128) over all 2880 visual tokens:
+            scores, tau, survivors, and the gather of their 4096-wide LLM hidden rows
+            and their key and value rows (32 x 128 each).
+Inputs are resident in HBM before timing starts.  lambda_1 / lambda_2 come from the
+budget matching of tests/golden/lambdas.json (523 and 40 kept tokens on average).
+
+Prints one JSON line: images/s, whole-step algorithmic HBM GB/s, the roofline entry of
+the dominant kernel (the Stage II scoring kernel, timed alone with HIP events on the
+stream it runs on) and the oracle's CPU throughput on a bounded sample.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import numpy as np  # noqa: E402
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, datasheet
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16, datasheet
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def stage_bytes(sb, kept_per_sample) -> dict:
+    """Algorithmic HBM bytes of one fused prune over a batch (per-image figures in the design doc).
+
+    keys: every key row once; queries once; scores written once (4 B per key);
+    gather: each survivor row read and written once; survivor lists 4 B each.
+    """
+    e = 2 if sb.dtype == "bf16" else 4
+    keys = int(sb.k_off[-1]) * sb.Hkv * sb.d * e
+    qry = int(sb.q_off[-1]) * sb.H * sb.d * e
+    score_w = int(sb.k_off[-1]) * 4
+    row_bytes = sum(pl.rows.shape[1] * pl.rows.itemsize for pl in sb.payload)
+    kept = int(np.sum(kept_per_sample))
+    gather = 2 * kept * row_bytes + 4 * kept
+    return dict(keys=keys, q=qry, scores=score_w, gather=gather,
+                total=keys + qry + score_w + gather)
+
+
+def cpu_baseline(name, lam1, lam2, budget_s=15.0, max_samples=256):
+    """The oracle on the host cores over the first samples of the workload, until ~budget_s."""
+    import oracle
+    from paper_2605_29657_amd import synth
+    oracle.build()
+    done, t_total = 0, 0.0
+    while done < max_samples and t_total < budget_s:
+        vis = synth.make_stage(name, "vis", samples=[done])
+        txt = synth.make_stage(name, "txt", samples=[done])
+        t0 = time.perf_counter()
+        for sb, lam in ((vis, lam1), (txt, lam2)):
+            scale = float(np.float32(1.0) / np.sqrt(np.float32(sb.d)))
+            res = oracle.prune(sb.q, sb.k, sb.q_off, sb.k_off, sb.H, sb.Hkv, sb.d, sb.R, lam,
+                               dtype=sb.dtype, scale=scale)
+            for pl in sb.payload:
+                oracle.gather(pl.rows, res["kept_idx"], res["kept_offsets"], sb.k_off, sb.R,
+                              src_pad_rows=pl.pad_rows, src_row0=pl.row0)
+        t_total += time.perf_counter() - t0
+        done += 1
+    cores = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    return {"value": done / t_total, "unit": "images/s", "cores": cores, "kind": "oracle",
+            "sample": "first %d image(s) of %s, both stages (scores, tau, survivors, gather), "
+                      "%.1f s" % (done, name, t_total)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llava_next")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--kernel-reps", type=int, default=20,
+                    help="timed repetitions of the dominant kernel alone")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the pruning path is per sample and needs no "
+              "communication; run it with --gpus 1 (see DESIGN.md for how it shards)",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2605_29657_amd import occam, synth
+    from paper_2605_29657_amd.runner import DeviceStage
+    from paper_2605_29657_amd.workloads import WORKLOADS
+
+    occam.lib()   # fail loudly if the HIP library is missing
+    torch.cuda.set_device(0)
+    name = args.workload
+    w = WORKLOADS[name]
+    with open(os.path.join(ROOT, "tests", "golden", "lambdas.json")) as f:
+        lams = json.load(f)[name]
+    lam1 = float(np.float32(lams["vis"]["lam"]))
+    lam2 = float(np.float32(lams["txt"]["lam"]))
+
+    t0 = time.time()
+    vis = synth.make_stage(name, "vis")
+    txt = synth.make_stage(name, "txt")
+    log("generated %s in %.1fs" % (name, time.time() - t0))
+    dv = DeviceStage(vis, ragged=vis.ragged)
+    dt = DeviceStage(txt, ragged=txt.ragged)
+    torch.cuda.synchronize()
+    B = vis.B
+
+    def step():
+        dv.prune(lam1)
+        dt.prune(lam2)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    kept1 = dv.out["kept_count"].cpu().numpy()
+    kept2 = dt.out["kept_count"].cpu().numpy()
+
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = e0.elapsed_time(e1) / args.steps
+    log("timed %d steps: %.3f ms/step (wall %.3f ms/step)" % (args.steps, ms,
+                                                              wall * 1e3 / args.steps))
+
+    b1 = stage_bytes(vis, kept1)
+    b2 = stage_bytes(txt, kept2)
+    step_bytes = b1["total"] + b2["total"]
+    images_s = B / (ms * 1e-3)
+    step_gbs = step_bytes / (ms * 1e-3) / 1e9
+
+    # Dominant kernel: the Stage II scoring kernel.  occam_score with a caller-supplied
+    # normaliser launches exactly that one kernel, so HIP events around the call on the
+    # launch stream time it alone.  The normaliser is the true per-(row, head) log-sum-exp
+    # (float32 matmul on the device; setup only).
+    lse = torch.empty(int(txt.q_off[-1]) * txt.H, dtype=torch.float32, device="cuda")
+    with torch.no_grad():
+        S = txt.R + int(txt.N[0])
+        T = int(txt.T[0])
+        grp = txt.H // txt.Hkv
+        for b in range(B):
+            qh = dt.q[b * T:(b + 1) * T].float().permute(1, 0, 2).contiguous()      # [H, T, d]
+            kh = dt.k[b * S:(b + 1) * S].float().repeat_interleave(grp, dim=1)
+            kh = kh.permute(1, 2, 0).contiguous()                                    # [H, d, S]
+            lg = torch.matmul(qh, kh) / float(np.sqrt(np.float32(txt.d)))            # [H, T, S]
+            lse.view(-1, txt.H)[b * T:(b + 1) * T] = torch.logsumexp(lg, dim=-1).transpose(0, 1)
+    scores_buf = torch.empty_like(dt.out["scores"])
+    occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws, row_lse=lse)
+    torch.cuda.synchronize()
+    k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    k0.record()
+    for _ in range(args.kernel_reps):
+        occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws, row_lse=lse)
+    k1.record()
+    torch.cuda.synchronize()
+    score_ms = k0.elapsed_time(k1) / args.kernel_reps
+    # Both Stage II passes (statistics + scoring) for reference.
+    k0.record()
+    for _ in range(args.kernel_reps):
+        occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws)
+    k1.record()
+    torch.cuda.synchronize()
+    both_ms = k0.elapsed_time(k1) / args.kernel_reps
+    kern_bytes = b2["keys"] + b2["q"] + b2["scores"]
+    achieved = kern_bytes / (score_ms * 1e-3) / 1e9
+    flops = 2.0 * int(txt.q_off[-1]) * txt.H * (txt.R + int(txt.N[0])) * txt.d
+    log("text_score alone %.3f ms (%.0f GB/s, %.0f TFLOP/s); stats+score %.3f ms" % (
+        score_ms, achieved, flops / (score_ms * 1e-3) / 1e12, both_ms))
+
+    traffic = None
+    tpath = os.path.join(ROOT, "profiles", "traffic.json")
+    if os.path.exists(tpath):
+        with open(tpath) as f:
+            tj = json.load(f)
+        if tj.get("kernel") == "text_score" and tj.get("workload") == name:
+            traffic = tj.get("bytes_per_launch")
+
+    rec = {
+        "metric": "images/s for fused prune at 2880 visual tokens; achieved HBM GB/s % of peak",
+        "value": round(images_s, 1),
+        "unit": "images/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "%s: B=%d, R=%d, N=%d visual tokens; Stage I CLS row H=16 d=64 "
+                               "+ 1024-wide hidden gather; Stage II %d text rows H=32 d=128 over "
+                               "all %d tokens + hidden/K/V gather" % (
+                                   name, B, w["R"], w["N"], w["txt"]["T"], w["N"]),
+                   "global_batch": B, "lambda1": lam1, "lambda2": lam2,
+                   "kept_stage1_mean": float(np.mean(kept1)),
+                   "kept_stage2_mean": float(np.mean(kept2))},
+        "achieved_hbm_gbs": round(step_gbs, 1),
+        "hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
+        "step_bytes": step_bytes,
+        "roofline": {"kernel": "text_score", "bound": "hbm", "achieved": round(achieved, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": traffic, "avg_ms": round(score_ms, 4),
+                     "bytes_per_launch": kern_bytes,
+                     "mfma_tflops": round(flops / (score_ms * 1e-3) / 1e12, 1),
+                     "mfma_frac": round(flops / (score_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+                     "stats_plus_score_ms": round(both_ms, 4)},
+    }
+    if not args.no_cpu_baseline:
+        rec["cpu_baseline"] = cpu_baseline(name, lam1, lam2)
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -4,8 +4,8 @@ TEST INFRASTRUCTURE ONLY.  The tests, the smoke check and the benchmark's CPU
 baseline leg are the only callers.  The GPU library neither imports nor links
 anything here, and nothing here imports the GPU library.
 
-The arithmetic lives in ``occam_oracle.c`` (double precision, plain loops, one
-OpenMP thread per sample); this module builds it with gcc, loads it with
+The arithmetic lives in ``occam_oracle.c`` (double precision, plain loops,
+OpenMP over the anchor rows of a sample); this module builds it with gcc, loads it with
 ctypes and adds two small numpy helpers that the paper defines outside the hot
 path:
 

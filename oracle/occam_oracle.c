@@ -93,23 +93,28 @@ int oracle_scores(int B, int H, int Hkv, int d, int R,
 
     const int group = H / Hkv;
     int err = 0;
-#pragma omp parallel for schedule(dynamic, 1)
     for (int b = 0; b < B; ++b) {
         const int64_t T = q_off[b + 1] - q_off[b];
         const int64_t S = k_off[b + 1] - k_off[b];
-        double *logit = (double *)malloc(sizeof(double) * (size_t)S);
+        /* abar[t][s]: head-mean attention of anchor row t to key s. */
         double *abar = (double *)calloc((size_t)(T * S), sizeof(double));
-        double *qrow = (double *)malloc(sizeof(double) * (size_t)d);
-        if (!logit || !abar || !qrow) {
+        if (!abar)
+            return -1;
+        /* Anchor rows are independent: one row per OpenMP task. */
+#pragma omp parallel for schedule(dynamic, 1)
+        for (int64_t t = 0; t < T; ++t) {
+            double *logit = (double *)malloc(sizeof(double) * (size_t)S);
+            double *qrow = (double *)malloc(sizeof(double) * (size_t)d);
+            if (!logit || !qrow) {
 #pragma omp atomic write
-            err = 1;
-            free(logit); free(abar); free(qrow);
-            continue;
-        }
-        for (int h = 0; h < H; ++h) {
-            const int g = h / group; /* key head read by query head h */
-            for (int64_t t = 0; t < T; ++t) {
-                const int64_t qrow_idx = q_off[b] + t;
+                err = 1;
+                free(logit); free(qrow);
+                continue;
+            }
+            const int64_t qrow_idx = q_off[b] + t;
+            double *arow = abar + t * S;
+            for (int h = 0; h < H; ++h) {
+                const int g = h / group; /* key head read by query head h */
                 for (int e = 0; e < d; ++e)
                     qrow[e] = load_elem(q, dtype, (qrow_idx * H + h) * d + e);
                 /* Step 1: l_s = scale * <q_t, k_s> (Eq. (1)). */
@@ -121,8 +126,8 @@ int oracle_scores(int B, int H, int Hkv, int d, int R,
                     logit[s] = scale * dot;
                 }
                 /* Step 2: A_s = softmax(l)_s over the S keys (Eq. (1)), or
-                 * exp(l_s - lse) with a caller-supplied normaliser. */
-                double *arow = abar + t * S;
+                 * exp(l_s - lse) with a caller-supplied normaliser; the head
+                 * mean accumulates A / H. */
                 if (row_lse) {
                     const double lse = row_lse[qrow_idx * H + h];
                     for (int64_t s = 0; s < S; ++s)
@@ -134,11 +139,12 @@ int oracle_scores(int B, int H, int Hkv, int d, int R,
                     double z = 0.0;
                     for (int64_t s = 0; s < S; ++s)
                         z += exp(logit[s] - m);
-                    /* head mean: accumulate A / H */
                     for (int64_t s = 0; s < S; ++s)
                         arow[s] += (exp(logit[s] - m) / z) / (double)H;
                 }
             }
+            free(logit);
+            free(qrow);
         }
         /* Step 3: visual score = max over anchor rows of the head-mean map;
          * register score = mean over anchor rows (Eq. text_scoring).  With one
@@ -157,9 +163,7 @@ int oracle_scores(int B, int H, int Hkv, int d, int R,
                 out[s] = mx;
             }
         }
-        free(logit);
         free(abar);
-        free(qrow);
     }
     return err ? -1 : 0;
 }

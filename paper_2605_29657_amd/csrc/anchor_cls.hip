@@ -1,0 +1,184 @@
+// Anchor path for one anchor row per sample (the CLS row of Stage I,
+// Eq. EQ:CLS), steps 1-2: logits of the CLS query against [registers ;
+// visual] keys (Eq. (1)), per-head softmax and the head mean (Appendix,
+// "Stage-I pruning": the vision map is averaged over heads).
+//
+// With a single query row the contraction is a matrix-vector product: every
+// key byte is used once, so the work is bound by HBM and runs on the VALU.
+//
+// cls_logits  grid (key chunk, sample): streams the chunk's key rows with
+//             coalesced 16-byte loads (a wave reads one key row per step,
+//             lane L reading bytes [16L, 16L+16) of it), forms per-16-byte
+//             partial dot products against the query held in LDS, sums them
+//             per (key, head), writes the scaled logits to the workspace and
+//             the chunk's per-head (max, sum exp) pair.
+// cls_scores  grid (key chunk, sample): merges the per-chunk pairs of the
+//             sample into the softmax normaliser of every head (fixed order),
+//             then score(s) = (1/H) sum_h exp(l[s,h] - m_h) / z_h.
+// Both kernels use fixed reduction orders, so results are run-to-run
+// identical.
+#include "occam_internal.hpp"
+
+namespace occam {
+
+template <bool BF16>
+__global__ __launch_bounds__(kClsThreads) void cls_logits_kernel(
+    Prob p, const void* __restrict__ qv, const void* __restrict__ kv,
+    float* __restrict__ logits, float2* __restrict__ stats, int kpw, int nchunks)
+{
+    extern __shared__ float smem[];
+    constexpr int CE = BF16 ? 8 : 4;            // elements per 16-byte chunk
+    const int c = blockIdx.x, b = blockIdx.y;
+    const int S = keys_of(p, b);
+    const int s0 = c * kpw;
+    if (s0 >= S) return;                        // uniform over the workgroup
+    const int nk = min(kpw, S - s0);
+    const int H = p.H, Hkv = p.Hkv, d = p.d, group = H / Hkv;
+    const int NC = d / CE;                      // chunks per key head
+    const int CPK = NC * Hkv;                   // chunks per key row
+    float* qs = smem;                           // [H][d]
+    int* tab = reinterpret_cast<int*>(qs + H * d);      // [CPK]: (g << 16) | part
+    float* part = reinterpret_cast<float*>(tab + CPK);  // [nk][H][NC]
+    float* lg = part + kpw * H * NC;                    // [nk][H]
+
+    const int qrow = q_begin(p, b);
+    if (BF16) {
+        const uint16_t* q16 = static_cast<const uint16_t*>(qv) + (size_t)qrow * H * d;
+        for (int i = threadIdx.x; i < H * d; i += blockDim.x)
+            qs[i] = __uint_as_float(static_cast<uint32_t>(q16[i]) << 16);
+    } else {
+        const float* q32 = static_cast<const float*>(qv) + (size_t)qrow * H * d;
+        for (int i = threadIdx.x; i < H * d; i += blockDim.x) qs[i] = q32[i];
+    }
+    for (int ci = threadIdx.x; ci < CPK; ci += blockDim.x)
+        tab[ci] = ((ci / NC) << 16) | (ci % NC);
+    __syncthreads();
+
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int nwave = blockDim.x / kWave;
+    const size_t row_elems = (size_t)Hkv * d;
+    const char* kbase = static_cast<const char*>(kv) +
+                        ((size_t)k_begin(p, b) + s0) * row_elems * (BF16 ? 2 : 4);
+    const size_t row_bytes = row_elems * (BF16 ? 2 : 4);
+    for (int key = wave; key < nk; key += nwave) {
+        const u32x4* krow = reinterpret_cast<const u32x4*>(kbase + (size_t)key * row_bytes);
+        for (int ci = lane; ci < CPK; ci += kWave) {
+            const u32x4 w = __builtin_nontemporal_load(krow + ci);
+            float kf[CE];
+            if (BF16) {
+                kf[0] = bf16_lo(w.x); kf[1] = bf16_hi(w.x);
+                kf[2] = bf16_lo(w.y); kf[3] = bf16_hi(w.y);
+                kf[4] = bf16_lo(w.z); kf[5] = bf16_hi(w.z);
+                kf[6] = bf16_lo(w.w); kf[7] = bf16_hi(w.w);
+            } else {
+                kf[0] = __uint_as_float(w.x); kf[1] = __uint_as_float(w.y);
+                kf[2] = __uint_as_float(w.z); kf[3] = __uint_as_float(w.w);
+            }
+            const int tg = tab[ci];
+            const int g = tg >> 16, pc = tg & 0xffff;
+            for (int i = 0; i < group; ++i) {
+                const int h = g * group + i;
+                const float* qq = qs + h * d + pc * CE;
+                float acc = 0.f;
+#pragma unroll
+                for (int e = 0; e < CE; ++e) acc = fmaf(qq[e], kf[e], acc);
+                part[(key * H + h) * NC + pc] = acc;
+            }
+        }
+    }
+    __syncthreads();
+
+    float* lout = logits + ((size_t)k_begin(p, b) + s0) * H;
+    for (int i = threadIdx.x; i < nk * H; i += blockDim.x) {
+        const float* pp = part + i * NC;
+        float acc = 0.f;
+        for (int e = 0; e < NC; ++e) acc += pp[e];
+        const float l = acc * p.scale;
+        lg[i] = l;
+        lout[i] = l;
+    }
+    __syncthreads();
+
+    for (int h = threadIdx.x; h < H; h += blockDim.x) {
+        float m = -INFINITY;
+        for (int key = 0; key < nk; ++key) m = fmaxf(m, lg[key * H + h]);
+        float z = 0.f;
+        for (int key = 0; key < nk; ++key) z += expf(lg[key * H + h] - m);
+        stats[((size_t)b * nchunks + c) * H + h] = make_float2(m, z);
+    }
+}
+
+__global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
+    Prob p, const float* __restrict__ logits, const float2* __restrict__ stats,
+    const float* __restrict__ row_lse, float* __restrict__ scores, int kpw, int nchunks)
+{
+    extern __shared__ float smem[];
+    const int c = blockIdx.x, b = blockIdx.y;
+    const int S = keys_of(p, b);
+    const int s0 = c * kpw;
+    if (s0 >= S) return;
+    const int nk = min(kpw, S - s0);
+    const int H = p.H;
+    float* mh = smem;       // [H] per-head max (or the caller's log normaliser)
+    float* zh = smem + H;   // [H] per-head sum of exp(l - m)
+    const int nch = (S + kpw - 1) / kpw;
+    for (int h = threadIdx.x; h < H; h += blockDim.x) {
+        if (row_lse) {
+            mh[h] = row_lse[(size_t)q_begin(p, b) * H + h];
+            zh[h] = 1.f;
+        } else {
+            const float2* st = stats + (size_t)b * nchunks * H + h;
+            float m = -INFINITY;
+            for (int j = 0; j < nch; ++j) m = fmaxf(m, st[(size_t)j * H].x);
+            float z = 0.f;
+            for (int j = 0; j < nch; ++j) {
+                const float2 v = st[(size_t)j * H];
+                z += v.y * expf(v.x - m);
+            }
+            mh[h] = m;
+            zh[h] = z;
+        }
+    }
+    __syncthreads();
+    const float* lrow = logits + ((size_t)k_begin(p, b) + s0) * H;
+    float* out = scores + k_begin(p, b) + s0;
+    const float invH = 1.f / (float)H;
+    for (int key = threadIdx.x; key < nk; key += blockDim.x) {
+        float acc = 0.f;
+        for (int h = 0; h < H; ++h) acc += expf(lrow[key * H + h] - mh[h]) / zh[h];
+        out[key] = acc * invH;
+    }
+}
+
+static size_t cls_logits_smem(const Prob& p, int bf16, int kpw) {
+    const int NC = p.d / (bf16 ? 8 : 4);
+    return sizeof(float) * ((size_t)p.H * p.d + (size_t)NC * p.Hkv + (size_t)kpw * p.H * NC +
+                            (size_t)kpw * p.H);
+}
+
+hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void* k,
+                             float* logits, float2* stats, int kpw, hipStream_t s)
+{
+    const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
+    dim3 grid(nchunks, p.B);
+    const size_t smem = cls_logits_smem(p, bf16, kpw);
+    if (bf16)
+        hipLaunchKernelGGL(cls_logits_kernel<true>, grid, dim3(kClsThreads), smem, s, p, q, k,
+                           logits, stats, kpw, nchunks);
+    else
+        hipLaunchKernelGGL(cls_logits_kernel<false>, grid, dim3(kClsThreads), smem, s, p, q, k,
+                           logits, stats, kpw, nchunks);
+    return hipGetLastError();
+}
+
+hipError_t launch_cls_scores(const Prob& p, const float* logits, const float2* stats,
+                             const float* row_lse, float* scores, int kpw, hipStream_t s)
+{
+    const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
+    dim3 grid(nchunks, p.B);
+    hipLaunchKernelGGL(cls_scores_kernel, grid, dim3(kClsThreads), 2 * p.H * sizeof(float), s, p,
+                       logits, stats, row_lse, scores, kpw, nchunks);
+    return hipGetLastError();
+}
+
+}  // namespace occam

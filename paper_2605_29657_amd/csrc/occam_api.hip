@@ -1,0 +1,255 @@
+// Host entry points of liboccam: argument validation, workspace layout and
+// kernel launches for the C ABI declared in include/occam.h.  Validation runs
+// before any HIP call, so an invalid call enqueues nothing.
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+
+#include "occam.h"
+#include "occam_internal.hpp"
+
+using namespace occam;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+struct Plan {
+    Prob p;
+    int bf16;
+    int text;          // 1: several anchor rows (MFMA path); 0: one anchor row (VALU path)
+    int kpw;           // keys per workgroup of the one-row path
+    size_t off_logits, off_stats, off_lse2, off_scores, off_tau, off_slot, total;
+};
+
+bool aligned(const void* ptr, size_t a) { return (reinterpret_cast<uintptr_t>(ptr) % a) == 0; }
+
+occam_status make_plan(const occam_problem* pr, Plan* pl) {
+    if (!pr) return OCCAM_ERR_INVALID_ARG;
+    const occam_problem& x = *pr;
+    if (x.batch < 1 || x.num_heads < 1 || x.num_kv_heads < 1 ||
+        x.num_heads % x.num_kv_heads != 0 || x.head_dim < 1 || x.head_dim > 256 ||
+        x.num_registers < 1 || x.num_registers > 32)
+        return OCCAM_ERR_INVALID_ARG;
+    if (x.dtype != OCCAM_F32 && x.dtype != OCCAM_BF16) return OCCAM_ERR_INVALID_ARG;
+    if (!(x.softmax_scale >= 0.f) || isinf(x.softmax_scale)) return OCCAM_ERR_INVALID_ARG;
+    const int max_rows = x.q_offsets ? x.max_rows : x.rows;
+    const int max_cands = x.key_offsets ? x.max_cands : x.cands;
+    if (max_rows < 1 || max_cands < 0) return OCCAM_ERR_INVALID_ARG;
+    if (x.q_offsets && !aligned(x.q_offsets, 4)) return OCCAM_ERR_INVALID_ARG;
+    if (x.key_offsets && !aligned(x.key_offsets, 4)) return OCCAM_ERR_INVALID_ARG;
+    const int bf16 = x.dtype == OCCAM_BF16;
+    const int H = x.num_heads, d = x.head_dim, R = x.num_registers, B = x.batch;
+    // Index arithmetic is 32-bit for counts and rows: keep every extent below 2^31.
+    const long long keys_cap = (long long)B * (R + (long long)max_cands);
+    const long long rows_cap = (long long)B * max_rows;
+    if (keys_cap * H >= (1LL << 31) || rows_cap * H >= (1LL << 31)) return OCCAM_ERR_UNSUPPORTED;
+    if (d % (bf16 ? 8 : 4) != 0) return OCCAM_ERR_UNSUPPORTED;
+
+    Plan P;
+    memset(&P, 0, sizeof P);
+    P.p.B = B; P.p.H = H; P.p.Hkv = x.num_kv_heads; P.p.d = d; P.p.R = R;
+    P.p.rows = x.rows; P.p.cands = x.cands;
+    P.p.q_off = x.q_offsets; P.p.k_off = x.key_offsets;
+    P.p.max_rows = max_rows; P.p.max_cands = max_cands;
+    P.p.scale = x.softmax_scale > 0.f ? x.softmax_scale : 1.0f / sqrtf((float)d);
+    P.bf16 = bf16;
+    P.text = max_rows > 1;
+    size_t off = 0;
+    if (P.text) {
+        if (!bf16 || d > 128) return OCCAM_ERR_UNSUPPORTED;
+        const size_t smem = (size_t)kTxtRows * (((d + 15) / 16) * 16 + 8) * 2 + (size_t)H * kTxtRows * 4;
+        if (smem > 65536) return OCCAM_ERR_UNSUPPORTED;
+        P.off_lse2 = off; off = align_up(off + (size_t)rows_cap * H * sizeof(float));
+    } else {
+        P.kpw = cls_keys_per_wg(H, d, bf16 ? 2 : 4);
+        const int NC = d / (bf16 ? 8 : 4);
+        const size_t smem = sizeof(float) * ((size_t)H * d + (size_t)NC * x.num_kv_heads +
+                                             (size_t)P.kpw * H * NC + (size_t)P.kpw * H);
+        if (smem > 65536) return OCCAM_ERR_UNSUPPORTED;
+        const long long nchunks = (R + (long long)max_cands + P.kpw - 1) / P.kpw;
+        P.off_logits = off; off = align_up(off + (size_t)keys_cap * H * sizeof(float));
+        P.off_stats = off; off = align_up(off + (size_t)B * nchunks * H * sizeof(float2));
+    }
+    P.off_scores = off; off = align_up(off + (size_t)keys_cap * sizeof(float));
+    P.off_tau = off; off = align_up(off + (size_t)B * sizeof(float));
+    P.off_slot = off; off = align_up(off + (size_t)B * max_cands * sizeof(int));
+    P.total = off;
+    *pl = P;
+    return OCCAM_OK;
+}
+
+template <typename T>
+T* ws_at(void* ws, size_t off) { return reinterpret_cast<T*>(static_cast<char*>(ws) + off); }
+
+occam_status check_ws(const Plan& P, void* ws, size_t ws_bytes) {
+    if (ws_bytes < P.total) return OCCAM_ERR_WORKSPACE;
+    if (!ws || !aligned(ws, kAlign)) return OCCAM_ERR_INVALID_ARG;
+    return OCCAM_OK;
+}
+
+bool lambda_ok(float lambda) { return lambda >= 0.f && !isinf(lambda); }
+bool reduce_ok(int32_t r) { return r == OCCAM_REG_MEAN || r == OCCAM_REG_MAX || r == OCCAM_REG_SUM; }
+
+occam_status rows_from(int32_t n, const occam_rows* t, RowTensors* out) {
+    memset(out, 0, sizeof *out);
+    if (n < 0 || n > OCCAM_MAX_ROW_TENSORS) return OCCAM_ERR_INVALID_ARG;
+    if (n > 0 && !t) return OCCAM_ERR_INVALID_ARG;
+    int vec = 1;
+    for (int i = 0; i < n; ++i) {
+        const occam_rows& r = t[i];
+        if (!r.src || !r.dst || r.row_bytes < 0 || r.src_pad_rows < 0 || r.src_row0 < 0 ||
+            r.src_row_stride_bytes < r.row_bytes || r.dst_row_stride_bytes < r.row_bytes)
+            return OCCAM_ERR_INVALID_ARG;
+        if (r.row_bytes % 4 || r.src_row_stride_bytes % 4 || r.dst_row_stride_bytes % 4 ||
+            !aligned(r.src, 4) || !aligned(r.dst, 4))
+            return OCCAM_ERR_INVALID_ARG;
+        if (r.row_bytes % 16 || r.src_row_stride_bytes % 16 || r.dst_row_stride_bytes % 16 ||
+            !aligned(r.src, 16) || !aligned(r.dst, 16))
+            vec = 0;
+        RowTensor& o = out->t[i];
+        o.src = static_cast<const char*>(r.src);
+        o.dst = static_cast<char*>(r.dst);
+        o.src_pad_rows = r.src_pad_rows;
+        o.src_row0 = r.src_row0;
+        o.src_stride = r.src_row_stride_bytes;
+        o.dst_stride = r.dst_row_stride_bytes;
+        o.row_bytes = r.row_bytes;
+    }
+    out->n = n;
+    out->vec16 = vec;
+    return OCCAM_OK;
+}
+
+inline occam_status hip_ok(hipError_t e) { return e == hipSuccess ? OCCAM_OK : OCCAM_ERR_HIP; }
+
+// Steps 1-2 into `scores` (device), both paths.
+occam_status run_score(const Plan& P, const void* q, const void* k, const float* row_lse,
+                       float* scores, void* ws, hipStream_t s) {
+    if (P.text) {
+        if (row_lse) return hip_ok(launch_text_score(P.p, q, k, row_lse, 1, scores, s));
+        float* lse2 = ws_at<float>(ws, P.off_lse2);
+        occam_status st = hip_ok(launch_text_stats(P.p, q, k, lse2, s));
+        if (st != OCCAM_OK) return st;
+        return hip_ok(launch_text_score(P.p, q, k, lse2, 0, scores, s));
+    }
+    float* logits = ws_at<float>(ws, P.off_logits);
+    float2* stats = ws_at<float2>(ws, P.off_stats);
+    occam_status st = hip_ok(launch_cls_logits(P.p, P.bf16, q, k, logits, stats, P.kpw, s));
+    if (st != OCCAM_OK) return st;
+    return hip_ok(launch_cls_scores(P.p, logits, stats, row_lse, scores, P.kpw, s));
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* occam_status_string(occam_status status) {
+    switch (status) {
+        case OCCAM_OK: return "OCCAM_OK";
+        case OCCAM_ERR_INVALID_ARG: return "OCCAM_ERR_INVALID_ARG: invalid argument";
+        case OCCAM_ERR_UNSUPPORTED: return "OCCAM_ERR_UNSUPPORTED: shape or type not supported";
+        case OCCAM_ERR_WORKSPACE: return "OCCAM_ERR_WORKSPACE: workspace too small";
+        case OCCAM_ERR_HIP: return "OCCAM_ERR_HIP: HIP runtime error";
+    }
+    return "unknown occam_status";
+}
+
+int32_t occam_version(void) { return OCCAM_VERSION; }
+
+size_t occam_workspace_size(const occam_problem* problem) {
+    Plan P;
+    if (make_plan(problem, &P) != OCCAM_OK) return 0;
+    return P.total;
+}
+
+occam_status occam_score(const occam_problem* problem, const void* q, const void* k,
+                         const float* row_lse, float* scores, void* workspace, size_t ws_bytes,
+                         hipStream_t stream) {
+    Plan P;
+    occam_status st = make_plan(problem, &P);
+    if (st != OCCAM_OK) return st;
+    if (!q || !k || !scores || !aligned(q, 16) || !aligned(k, 16) || !aligned(scores, 4) ||
+        (row_lse && !aligned(row_lse, 4)))
+        return OCCAM_ERR_INVALID_ARG;
+    if ((st = check_ws(P, workspace, ws_bytes)) != OCCAM_OK) return st;
+    return run_score(P, q, k, row_lse, scores, workspace, stream);
+}
+
+occam_status occam_threshold(const occam_problem* problem, const float* scores, float lambda,
+                             int32_t reduce, float* tau, hipStream_t stream) {
+    Plan P;
+    occam_status st = make_plan(problem, &P);
+    if (st != OCCAM_OK) return st;
+    if (!scores || !tau || !aligned(scores, 4) || !aligned(tau, 4) || !lambda_ok(lambda) ||
+        !reduce_ok(reduce))
+        return OCCAM_ERR_INVALID_ARG;
+    return hip_ok(launch_threshold(P.p, scores, lambda, reduce, tau, stream));
+}
+
+occam_status occam_select(const occam_problem* problem, const float* scores, const float* tau,
+                          const int32_t* index_map, int32_t* kept_idx, int32_t* kept_count,
+                          int32_t* kept_offsets, void* workspace, size_t ws_bytes,
+                          hipStream_t stream) {
+    Plan P;
+    occam_status st = make_plan(problem, &P);
+    if (st != OCCAM_OK) return st;
+    if (!scores || !tau || !kept_idx || !kept_count || !kept_offsets || !aligned(scores, 4) ||
+        !aligned(tau, 4) || !aligned(kept_idx, 4) || !aligned(kept_count, 4) ||
+        !aligned(kept_offsets, 4) || (index_map && !aligned(index_map, 4)))
+        return OCCAM_ERR_INVALID_ARG;
+    if ((st = check_ws(P, workspace, ws_bytes)) != OCCAM_OK) return st;
+    int* slot = ws_at<int>(workspace, P.off_slot);
+    st = hip_ok(launch_select(P.p, scores, tau, 0, 0.f, 0, nullptr, slot, kept_count, stream));
+    if (st != OCCAM_OK) return st;
+    RowTensors none;
+    memset(&none, 0, sizeof none);
+    return hip_ok(launch_pack_gather(P.p, slot, kept_count, index_map, kept_idx, kept_offsets,
+                                     nullptr, nullptr, none, stream));
+}
+
+occam_status occam_gather(const occam_problem* problem, int32_t n, const occam_rows* tensors,
+                          const int32_t* kept_idx, const int32_t* kept_offsets,
+                          hipStream_t stream) {
+    Plan P;
+    occam_status st = make_plan(problem, &P);
+    if (st != OCCAM_OK) return st;
+    RowTensors rows;
+    if ((st = rows_from(n, tensors, &rows)) != OCCAM_OK) return st;
+    if (!kept_idx || !kept_offsets || !aligned(kept_idx, 4) || !aligned(kept_offsets, 4))
+        return OCCAM_ERR_INVALID_ARG;
+    if (n == 0) return OCCAM_OK;
+    return hip_ok(launch_pack_gather(P.p, nullptr, nullptr, nullptr, nullptr, nullptr, kept_idx,
+                                     kept_offsets, rows, stream));
+}
+
+occam_status occam_prune(const occam_problem* problem, const void* q, const void* k,
+                         const float* row_lse, float lambda, int32_t reduce,
+                         const int32_t* index_map, int32_t n, const occam_rows* tensors,
+                         float* scores, float* tau, int32_t* kept_idx, int32_t* kept_count,
+                         int32_t* kept_offsets, void* workspace, size_t ws_bytes,
+                         hipStream_t stream) {
+    Plan P;
+    occam_status st = make_plan(problem, &P);
+    if (st != OCCAM_OK) return st;
+    if (!q || !k || !kept_idx || !kept_count || !kept_offsets || !aligned(q, 16) ||
+        !aligned(k, 16) || !aligned(kept_idx, 4) || !aligned(kept_count, 4) ||
+        !aligned(kept_offsets, 4) || (scores && !aligned(scores, 4)) || (tau && !aligned(tau, 4)) ||
+        (row_lse && !aligned(row_lse, 4)) || (index_map && !aligned(index_map, 4)) ||
+        !lambda_ok(lambda) || !reduce_ok(reduce))
+        return OCCAM_ERR_INVALID_ARG;
+    RowTensors rows;
+    if ((st = rows_from(n, tensors, &rows)) != OCCAM_OK) return st;
+    if ((st = check_ws(P, workspace, ws_bytes)) != OCCAM_OK) return st;
+    float* sc = scores ? scores : ws_at<float>(workspace, P.off_scores);
+    float* tu = tau ? tau : ws_at<float>(workspace, P.off_tau);
+    int* slot = ws_at<int>(workspace, P.off_slot);
+    if ((st = run_score(P, q, k, row_lse, sc, workspace, stream)) != OCCAM_OK) return st;
+    st = hip_ok(launch_select(P.p, sc, nullptr, 1, lambda, reduce, tu, slot, kept_count, stream));
+    if (st != OCCAM_OK) return st;
+    return hip_ok(launch_pack_gather(P.p, slot, kept_count, index_map, kept_idx, kept_offsets,
+                                     nullptr, nullptr, rows, stream));
+}
+
+}  // extern "C"

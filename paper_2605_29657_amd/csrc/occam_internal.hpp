@@ -1,0 +1,110 @@
+// Internal definitions shared by the HIP kernels and the host entry points of
+// liboccam (gfx950 / CDNA4, wave64).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace occam {
+
+constexpr int kWave = 64;
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Problem view passed by value to every kernel.  Offsets are device pointers
+// or null (uniform batch).
+struct Prob {
+    int B, H, Hkv, d, R;
+    int rows, cands;          // uniform T and N (used when the offsets are null)
+    const int* q_off;         // [B+1] prefix of T_b, or null
+    const int* k_off;         // [B+1] prefix of R + N_b, or null
+    int max_rows, max_cands;  // bounds of T_b and N_b
+    float scale;              // softmax temperature of Eq. (1)
+};
+
+__device__ __forceinline__ int q_begin(const Prob& p, int b) {
+    return p.q_off ? p.q_off[b] : b * p.rows;
+}
+__device__ __forceinline__ int rows_of(const Prob& p, int b) {
+    if (!p.q_off) return p.rows;
+    int t = p.q_off[b + 1] - p.q_off[b];
+    return t < p.max_rows ? t : p.max_rows;
+}
+__device__ __forceinline__ int k_begin(const Prob& p, int b) {
+    return p.k_off ? p.k_off[b] : b * (p.R + p.cands);
+}
+// Keys of sample b (registers + visual), clamped to the launch bounds.
+__device__ __forceinline__ int keys_of(const Prob& p, int b) {
+    if (!p.k_off) return p.R + p.cands;
+    int s = p.k_off[b + 1] - p.k_off[b];
+    int hi = p.R + p.max_cands;
+    s = s < hi ? s : hi;
+    return s > p.R ? s : p.R;
+}
+// Visual tokens of the samples before b (indexes index_map and gather sources).
+__device__ __forceinline__ int cand_begin(const Prob& p, int b) {
+    return k_begin(p, b) - p.R * b;
+}
+
+// bf16 <-> f32 on raw 16-bit patterns.
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
+
+// Row tensors gathered with the survivors (host struct occam_rows, by value).
+constexpr int kMaxRowTensors = 8;
+struct RowTensor {
+    const char* src;
+    char* dst;
+    long long src_pad_rows, src_row0, src_stride, dst_stride, row_bytes;
+};
+struct RowTensors {
+    RowTensor t[kMaxRowTensors];
+    int n;
+    int vec16;  // every pointer, stride and row length is a multiple of 16 bytes
+};
+
+// ---------------------------------------------------------------------------
+// Tiling constants.
+// Anchor (T = 1) path: VALU dot products, KPW keys per workgroup.
+constexpr int kClsThreads = 256;
+constexpr int kClsPartials = 8192;   // LDS floats of per-chunk partial dot products
+// Text (T > 1) path: MFMA 32x32x16 bf16; 4 waves; a t-block of 128 anchor rows
+// (4 sub-blocks of 32) and 32 keys per wave.
+constexpr int kTxtThreads = 256;
+constexpr int kTxtRows = 128;
+constexpr int kTxtKeysPerWave = 32;
+constexpr int kTxtKeysPerWg = kTxtKeysPerWave * (kTxtThreads / kWave);
+constexpr int kSelThreads = 256;
+constexpr int kGatherThreads = 256;
+
+// Anchor-path keys per workgroup for a given row geometry.
+inline int cls_keys_per_wg(int H, int d, int elem_bytes) {
+    int chunks_per_head = d * elem_bytes / 16;
+    int kpw = kClsPartials / (H * chunks_per_head);
+    if (kpw > 64) kpw = 64;
+    if (kpw < 1) kpw = 1;
+    return kpw;
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (defined in the .hip files).  All return hipGetLastError().
+hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void* k,
+                             float* logits, float2* stats, int kpw, hipStream_t s);
+hipError_t launch_cls_scores(const Prob& p, const float* logits, const float2* stats,
+                             const float* row_lse, float* scores, int kpw, hipStream_t s);
+hipError_t launch_text_stats(const Prob& p, const void* q, const void* k, float* lse2,
+                             hipStream_t s);
+hipError_t launch_text_score(const Prob& p, const void* q, const void* k, const float* lse,
+                             int lse_natural, float* scores, hipStream_t s);
+hipError_t launch_threshold(const Prob& p, const float* scores, float lambda, int reduce,
+                            float* tau, hipStream_t s);
+hipError_t launch_select(const Prob& p, const float* scores, const float* tau, int fuse_tau,
+                         float lambda, int reduce, float* tau_out, int* slot, int* count,
+                         hipStream_t s);
+hipError_t launch_pack_gather(const Prob& p, const int* slot, const int* count,
+                              const int* index_map, int* kept_idx, int* kept_offsets,
+                              const int* packed_idx, const int* packed_offsets,
+                              const RowTensors& rows, hipStream_t s);
+
+}  // namespace occam

@@ -1,0 +1,182 @@
+// Steps 3-5 of the relative evidence test: the register-anchored threshold
+// (Eqs. stage1_threshold_appendix, stage2_set_appendix), the >= test of
+// Eqs. stage1 / stage2, the ascending compaction of the survivors, and the
+// dense copy of their rows that forms the pruned sequence of Algorithm 1.
+//
+// threshold    one thread per sample: tau = lambda * reduce(register scores).
+// select       one workgroup per sample: each 256-candidate step evaluates the
+//              test, takes a wave ballot, ranks lanes with mbcnt and the
+//              waves with a 4-entry LDS scan, and appends the survivors'
+//              candidate-local indices, ascending, to the sample's slot of
+//              the workspace (slot[co_b + i]).  Optionally computes tau first.
+// pack_gather  grid (G, sample): every workgroup forms its sample's packed
+//              offset (exclusive sum of the counts before it), writes the
+//              packed survivor list (through index_map when given) and
+//              kept_offsets, and its waves copy survivor rows of every row
+//              tensor with 16-byte vector loads and stores.
+#include "occam_internal.hpp"
+
+namespace occam {
+
+__device__ __forceinline__ float reg_reduce(const float* s, int R, int reduce) {
+    if (reduce == 1) {                     // OCCAM_REG_MAX
+        float m = s[0];
+        for (int r = 1; r < R; ++r) m = fmaxf(m, s[r]);
+        return m;
+    }
+    float acc = 0.f;
+    for (int r = 0; r < R; ++r) acc += s[r];
+    return reduce == 0 ? acc / (float)R : acc;   // MEAN : SUM
+}
+
+__global__ void threshold_kernel(Prob p, const float* __restrict__ scores, float lambda,
+                                 int reduce, float* __restrict__ tau)
+{
+    const int b = blockIdx.x * blockDim.x + threadIdx.x;
+    if (b >= p.B) return;
+    tau[b] = lambda * reg_reduce(scores + k_begin(p, b), p.R, reduce);
+}
+
+__global__ __launch_bounds__(kSelThreads) void select_kernel(
+    Prob p, const float* __restrict__ scores, const float* __restrict__ tau_in, int fuse_tau,
+    float lambda, int reduce, float* __restrict__ tau_out, int* __restrict__ slot,
+    int* __restrict__ count)
+{
+    __shared__ int wcount[kSelThreads / kWave];
+    __shared__ float tau_s;
+    const int b = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int kb = k_begin(p, b);
+    const int N = keys_of(p, b) - p.R;
+    const int co = cand_begin(p, b);
+    if (tid == 0) {
+        float t;
+        if (fuse_tau) {
+            t = lambda * reg_reduce(scores + kb, p.R, reduce);
+            if (tau_out) tau_out[b] = t;
+        } else {
+            t = tau_in[b];
+        }
+        tau_s = t;
+    }
+    __syncthreads();
+    const float tau = tau_s;
+    const float* sv = scores + kb + p.R;
+    int base = 0;
+    for (int v0 = 0; v0 < N; v0 += kSelThreads) {
+        const int v = v0 + tid;
+        const bool keep = v < N && sv[v] >= tau;
+        const unsigned long long mask = __ballot(keep);
+        const int pos = __builtin_amdgcn_mbcnt_hi((unsigned)(mask >> 32),
+                                                  __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0u));
+        if (lane == 0) wcount[wave] = __popcll(mask);
+        __syncthreads();
+        int pre = 0, tot = 0;
+#pragma unroll
+        for (int w = 0; w < kSelThreads / kWave; ++w) {
+            const int cw = wcount[w];
+            pre += w < wave ? cw : 0;
+            tot += cw;
+        }
+        if (keep) slot[co + base + pre + pos] = v;
+        base += tot;
+        __syncthreads();
+    }
+    if (tid == 0) count[b] = base;
+}
+
+__global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
+    Prob p, const int* __restrict__ slot, const int* __restrict__ count,
+    const int* __restrict__ index_map, int* __restrict__ kept_idx, int* __restrict__ kept_offsets,
+    const int* __restrict__ packed_idx, const int* __restrict__ packed_offsets, RowTensors rows)
+{
+    __shared__ int red[kGatherThreads];
+    const int b = blockIdx.y, x = blockIdx.x, G = gridDim.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int co = cand_begin(p, b);
+    int off, cnt;
+    const int* idx;
+    if (packed_idx) {
+        off = packed_offsets[b];
+        cnt = packed_offsets[b + 1] - off;
+        idx = packed_idx + off;
+    } else {
+        int acc = 0;
+        for (int j = tid; j < b; j += kGatherThreads) acc += count[j];
+        red[tid] = acc;
+        __syncthreads();
+        for (int s = kGatherThreads / 2; s > 0; s >>= 1) {
+            if (tid < s) red[tid] += red[tid + s];
+            __syncthreads();
+        }
+        off = red[0];
+        cnt = count[b];
+        idx = slot + co;
+        if (x == 0 && tid == 0) {
+            kept_offsets[b] = off;
+            if (b == p.B - 1) kept_offsets[p.B] = off + cnt;
+        }
+        for (int i = x * kGatherThreads + tid; i < cnt; i += G * kGatherThreads) {
+            const int v = idx[i];
+            kept_idx[off + i] = index_map ? index_map[co + v] : v;
+        }
+    }
+    const int nt = rows.n;
+    if (nt == 0) return;
+    const int jobs = cnt * nt;
+    const int nw = kGatherThreads / kWave;
+    for (int j = x * nw + wave; j < jobs; j += G * nw) {
+        const int i = j / nt, t = j - i * nt;
+        const int v = idx[i];
+        const RowTensor& rt = rows.t[t];
+        const char* src = rt.src + ((long long)co + (long long)b * rt.src_pad_rows + rt.src_row0 + v) *
+                                       rt.src_stride;
+        char* dst = rt.dst + (long long)(off + i) * rt.dst_stride;
+        const long long nb = rt.row_bytes;
+        if (rows.vec16) {
+            for (long long o = (long long)lane * 16; o < nb; o += 16 * kWave)
+                *reinterpret_cast<uint4*>(dst + o) = *reinterpret_cast<const uint4*>(src + o);
+        } else {
+            for (long long o = (long long)lane * 4; o < nb; o += 4 * kWave)
+                *reinterpret_cast<uint32_t*>(dst + o) = *reinterpret_cast<const uint32_t*>(src + o);
+        }
+    }
+}
+
+hipError_t launch_threshold(const Prob& p, const float* scores, float lambda, int reduce,
+                            float* tau, hipStream_t s)
+{
+    hipLaunchKernelGGL(threshold_kernel, dim3((p.B + 255) / 256), dim3(256), 0, s, p, scores,
+                       lambda, reduce, tau);
+    return hipGetLastError();
+}
+
+hipError_t launch_select(const Prob& p, const float* scores, const float* tau, int fuse_tau,
+                         float lambda, int reduce, float* tau_out, int* slot, int* count,
+                         hipStream_t s)
+{
+    hipLaunchKernelGGL(select_kernel, dim3(p.B), dim3(kSelThreads), 0, s, p, scores, tau, fuse_tau,
+                       lambda, reduce, tau_out, slot, count);
+    return hipGetLastError();
+}
+
+hipError_t launch_pack_gather(const Prob& p, const int* slot, const int* count,
+                              const int* index_map, int* kept_idx, int* kept_offsets,
+                              const int* packed_idx, const int* packed_offsets,
+                              const RowTensors& rows, hipStream_t s)
+{
+    // Enough workgroups per sample to cover the worst-case survivor count with
+    // one row per wave, but no more than ~2048 in total.
+    const int nw = kGatherThreads / kWave;
+    long long per = rows.n > 0 ? ((long long)p.max_cands * rows.n + nw - 1) / nw
+                               : ((long long)p.max_cands + kGatherThreads - 1) / kGatherThreads;
+    long long cap = (2048 + p.B - 1) / p.B;
+    long long G = per < cap ? per : cap;
+    if (G < 1) G = 1;
+    hipLaunchKernelGGL(pack_gather_kernel, dim3((unsigned)G, p.B), dim3(kGatherThreads), 0, s, p,
+                       slot, count, index_map, kept_idx, kept_offsets, packed_idx, packed_offsets,
+                       rows);
+    return hipGetLastError();
+}
+
+}  // namespace occam

@@ -1,0 +1,178 @@
+"""The C ABI library on the CPU: it loads, exports every symbol include/occam.h declares,
+and rejects invalid arguments on the host before anything is enqueued.
+
+No call here reaches a kernel launch: every case carries at least one invalid
+argument, and validation runs before any HIP call.
+"""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_2605_29657_amd import build as occam_build
+from paper_2605_29657_amd import occam
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "occam.h")
+FAKE = 0x7f0000000000          # a 256-byte aligned, never-dereferenced "device" address
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(occam.LIB_PATH):
+        occam_build.build()
+    return occam.lib()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(occam_[a-z_]+)\s*\(", text)))
+
+
+def test_header_declares_the_five_steps_and_helpers():
+    names = declared_functions()
+    for fn in ("occam_score", "occam_threshold", "occam_select", "occam_gather", "occam_prune",
+               "occam_workspace_size", "occam_status_string", "occam_version"):
+        assert fn in names
+    assert set(names) == set(occam.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol(L):
+    out = subprocess.run(["nm", "-D", "--defined-only", occam.LIB_PATH], capture_output=True,
+                         text=True, check=True).stdout
+    exported = set(re.findall(r"\bT (occam_\w+)", out))
+    for fn in declared_functions():
+        assert fn in exported, fn
+        assert hasattr(L, fn)
+
+
+def test_version_and_status_strings(L):
+    assert L.occam_version() == 1
+    for s in range(5):
+        assert occam.status_string(s).startswith("OCCAM_")
+    assert "unknown" in occam.status_string(77)
+
+
+def good_problem(**kw):
+    args = dict(batch=4, num_heads=16, num_kv_heads=16, head_dim=64, num_registers=4, rows=1,
+                cands=576, dtype=occam.BF16)
+    args.update(kw)
+    return occam.Problem(**args)
+
+
+def ws_size(p):
+    return occam.workspace_size(p)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(batch=0), dict(num_heads=0), dict(num_kv_heads=0), dict(num_heads=16, num_kv_heads=5),
+    dict(head_dim=0), dict(head_dim=264), dict(num_registers=0), dict(num_registers=33),
+    dict(rows=0), dict(cands=-1), dict(dtype=7), dict(softmax_scale=-1.0),
+    dict(softmax_scale=float("inf")), dict(softmax_scale=float("nan")),
+])
+def test_invalid_problems(L, kw):
+    p = good_problem(**kw)
+    assert ws_size(p) == 0
+    st = L.occam_score(p.ref, FAKE, FAKE, None, FAKE, FAKE, 1 << 40, None)
+    assert st == occam.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("kw", [
+    dict(dtype=occam.F32, rows=8, num_heads=32, num_kv_heads=32, head_dim=128),   # f32 text rows
+    dict(head_dim=6),                                                              # bf16 needs d % 8
+    dict(dtype=occam.F32, head_dim=6),                                             # f32 needs d % 4
+    dict(rows=64, head_dim=136),                                                   # text rows: d <= 128
+])
+def test_unsupported_shapes(L, kw):
+    p = good_problem(**kw)
+    assert ws_size(p) == 0
+    st = L.occam_score(p.ref, FAKE, FAKE, None, FAKE, FAKE, 1 << 40, None)
+    assert st == occam.ERR_UNSUPPORTED
+
+
+def test_workspace_size_grows_with_the_batch(L):
+    small = ws_size(good_problem(batch=1))
+    big = ws_size(good_problem(batch=64))
+    assert 0 < small < big
+    txt = ws_size(good_problem(rows=128, num_heads=32, num_kv_heads=32, head_dim=128, cands=2880))
+    assert txt > 0
+
+
+def test_ragged_problem_needs_bounds(L):
+    p = occam.Problem(4, 16, 16, 64, 4, q_offsets=FAKE, key_offsets=FAKE, max_rows=0,
+                      max_cands=100, dtype=occam.BF16)
+    assert ws_size(p) == 0
+    p = occam.Problem(4, 16, 16, 64, 4, q_offsets=FAKE, key_offsets=FAKE, max_rows=1,
+                      max_cands=100, dtype=occam.BF16)
+    assert ws_size(p) > 0
+    p = occam.Problem(4, 16, 16, 64, 4, q_offsets=FAKE + 2, key_offsets=FAKE, max_rows=1,
+                      max_cands=100, dtype=occam.BF16)
+    assert ws_size(p) == 0
+
+
+def test_score_argument_checks(L):
+    p = good_problem()
+    n = ws_size(p)
+    assert L.occam_score(p.ref, None, FAKE, None, FAKE, FAKE, n, None) == occam.ERR_INVALID_ARG
+    assert L.occam_score(p.ref, FAKE + 8, FAKE, None, FAKE, FAKE, n, None) == occam.ERR_INVALID_ARG
+    assert L.occam_score(p.ref, FAKE, FAKE, None, None, FAKE, n, None) == occam.ERR_INVALID_ARG
+    assert L.occam_score(p.ref, FAKE, FAKE, None, FAKE, FAKE, n - 1, None) == occam.ERR_WORKSPACE
+    assert L.occam_score(p.ref, FAKE, FAKE, None, FAKE, FAKE + 64, n, None) == occam.ERR_INVALID_ARG
+    assert L.occam_score(None, FAKE, FAKE, None, FAKE, FAKE, n, None) == occam.ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("lam", [-0.5, float("nan"), float("inf")])
+def test_threshold_and_prune_reject_bad_lambda(L, lam):
+    p = good_problem()
+    assert L.occam_threshold(p.ref, FAKE, lam, 0, FAKE, None) == occam.ERR_INVALID_ARG
+    st = L.occam_prune(p.ref, FAKE, FAKE, None, lam, 0, None, 0, None, None, None, FAKE, FAKE,
+                       FAKE, FAKE, ws_size(p), None)
+    assert st == occam.ERR_INVALID_ARG
+
+
+def test_reduce_mode_is_checked(L):
+    p = good_problem()
+    assert L.occam_threshold(p.ref, FAKE, 0.5, 3, FAKE, None) == occam.ERR_INVALID_ARG
+
+
+def test_select_argument_checks(L):
+    p = good_problem()
+    n = ws_size(p)
+    assert L.occam_select(p.ref, FAKE, FAKE, None, None, FAKE, FAKE, FAKE, n, None) == \
+        occam.ERR_INVALID_ARG
+    assert L.occam_select(p.ref, FAKE, FAKE, FAKE + 2, FAKE, FAKE, FAKE, FAKE, n, None) == \
+        occam.ERR_INVALID_ARG
+    assert L.occam_select(p.ref, FAKE, FAKE, None, FAKE, FAKE, FAKE, FAKE, 16, None) == \
+        occam.ERR_WORKSPACE
+
+
+def rows_array(*items):
+    arr = (occam._Rows * len(items))(*items)
+    return arr
+
+
+def test_gather_row_descriptor_checks(L):
+    p = good_problem()
+    ok = occam._Rows(FAKE, FAKE, 0, 0, 2048, 2048, 2048)
+    bad_stride = occam._Rows(FAKE, FAKE, 0, 0, 1024, 2048, 2048)     # stride < row bytes
+    bad_align = occam._Rows(FAKE + 2, FAKE, 0, 0, 2048, 2048, 2048)  # src not 4-byte aligned
+    bad_len = occam._Rows(FAKE, FAKE, 0, 0, 2048, 2048, 2046)        # row bytes % 4
+    neg_pad = occam._Rows(FAKE, FAKE, -1, 0, 2048, 2048, 2048)
+    for r in (bad_stride, bad_align, bad_len, neg_pad):
+        assert L.occam_gather(p.ref, 1, rows_array(r), FAKE, FAKE, None) == occam.ERR_INVALID_ARG
+    assert L.occam_gather(p.ref, 9, rows_array(*([ok] * 9)), FAKE, FAKE, None) == \
+        occam.ERR_INVALID_ARG
+    assert L.occam_gather(p.ref, 1, None, FAKE, FAKE, None) == occam.ERR_INVALID_ARG
+    assert L.occam_gather(p.ref, 1, rows_array(ok), None, FAKE, None) == occam.ERR_INVALID_ARG
+    # n = 0 is a valid no-op that enqueues nothing.
+    assert L.occam_gather(p.ref, 0, None, FAKE, FAKE, None) == occam.OK
+
+
+def test_binding_raises_without_the_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(occam, "_lib", None)
+    monkeypatch.setattr(occam, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(RuntimeError):
+        occam.lib()

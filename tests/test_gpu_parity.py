@@ -1,0 +1,251 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle.
+
+Every workload shape is checked on seeded synthetic inputs: small batches element by
+element, the headline LLaVA-NeXT batch at full size in the launch configuration the
+benchmark times (sampled samples), plus edge cases (empty and ragged samples, all or
+no survivors, several t-blocks, GQA, d % 16 == 8, other register reductions), the
+unfused entry points, determinism, the caller-normaliser mode and index remapping.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2605_29657_amd import occam, synth
+from paper_2605_29657_amd.runner import DeviceStage, to_device
+
+from parity import (RTOL, check_bookkeeping, check_rows, check_scores, check_selection, custom_stage, f32_scale,
+                    lam_for, oracle_prune)
+
+pytestmark = pytest.mark.gpu
+
+
+def run_and_check(sb, lam, reduce=oracle.REG_MEAN, ragged=None, rows=True):
+    print("case: %s/%s B=%d R=%d H=%d Hkv=%d d=%d T=%s N=%s dtype=%s lam=%.6g ragged=%s" % (
+        sb.workload, sb.stage, sb.B, sb.R, sb.H, sb.Hkv, sb.d, sb.T[:4], sb.N[:4], sb.dtype, lam,
+        ragged), flush=True)
+    ds = DeviceStage(sb, ragged=ragged)
+    ds.prune(lam, reduce=reduce, with_rows=rows)
+    g = ds.host(with_rows=rows)
+    o = oracle_prune(sb, lam, reduce=reduce)
+    rtol = RTOL[sb.dtype]
+    err = check_scores(g["scores"], o["scores"], rtol)
+    check_scores(g["tau"], o["tau"], rtol, "tau")
+    sel = check_selection(g, o, sb, rtol)
+    if rows:
+        check_rows(g, sb)
+    print("  max rel score err %.3g, kept %d, exempt %d" % (err, sel["kept"], sel["exempt"]),
+          flush=True)
+    return g, o
+
+
+# ----------------------------------------------------------------------------- workloads
+@pytest.mark.parametrize("ragged", [False, True])
+def test_llava15_cls_f32(ragged):
+    sb = synth.make_stage("llava15_cls_f32", "vis")
+    run_and_check(sb, lam_for("llava15_cls_f32", "vis"), ragged=ragged)
+
+
+@pytest.mark.parametrize("stage", ["vis", "txt"])
+def test_llava15(stage):
+    sb = synth.make_stage("llava15", stage, B=4)
+    run_and_check(sb, lam_for("llava15", stage))
+
+
+@pytest.mark.parametrize("stage", ["vis", "txt"])
+def test_llava_next(stage):
+    sb = synth.make_stage("llava_next", stage, B=2)
+    run_and_check(sb, lam_for("llava_next", stage))
+
+
+@pytest.mark.parametrize("stage", ["vis", "txt"])
+def test_qwen3vl_ragged(stage):
+    sb = synth.make_stage("qwen3vl_ragged", stage, B=5)
+    assert sb.ragged
+    run_and_check(sb, lam_for("qwen3vl_ragged", stage))
+
+
+@pytest.mark.parametrize("stage", ["vis", "txt"])
+def test_video_full_sample(stage):
+    sb = synth.make_stage("video", stage, B=1)
+    run_and_check(sb, lam_for("video", stage))
+
+
+@pytest.mark.parametrize("stage", ["vis", "txt"])
+def test_headline_full_batch_sampled(stage):
+    # The LLaVA-NeXT batch at full size (B=32), uniform launch as the benchmark runs it;
+    # three samples are recomputed by the oracle (a sample's bytes do not depend on B).
+    name = "llava_next"
+    lam = lam_for(name, stage)
+    sb = synth.make_stage(name, stage)
+    ds = DeviceStage(sb, ragged=False)
+    ds.prune(lam)
+    g = ds.host()
+    pick = [0, 17, 31]
+    sub = synth.make_stage(name, stage, samples=pick)
+    o = oracle_prune(sub, lam)
+    rtol = RTOL[sb.dtype]
+    for j, b in enumerate(pick):
+        gs = g["scores"][sb.k_off[b]:sb.k_off[b + 1]]
+        check_scores(gs, o["scores"][sub.k_off[j]:sub.k_off[j + 1]], rtol)
+        check_scores(g["tau"][b:b + 1], o["tau"][j:j + 1], rtol, "tau")
+        gsel = dict(kept_idx=g["kept_idx"][g["kept_offsets"][b]:g["kept_offsets"][b + 1]],
+                    kept_count=g["kept_count"][b:b + 1],
+                    kept_offsets=np.array([0, g["kept_count"][b]]))
+        one = synth.make_stage(name, stage, samples=[b], payload=False)
+        oj = dict(scores=o["scores"][sub.k_off[j]:sub.k_off[j + 1]], tau=o["tau"][j:j + 1],
+                  kept_idx=o["kept_idx"][o["kept_offsets"][j]:o["kept_offsets"][j + 1]],
+                  kept_offsets=np.array([0, o["kept_count"][j]]))
+        check_selection(gsel, oj, one, rtol)
+    # Whole-batch properties at full size: bookkeeping and byte-exact rows.
+    check_bookkeeping(g, sb)
+    check_rows(g, sb)
+
+
+# ----------------------------------------------------------------------------- edge cases
+def test_ragged_with_empty_samples():
+    sb = custom_stage(B=5, R=3, H=4, Hkv=4, d=64, T=[1] * 5, N=[0, 37, 0, 300, 1])
+    run_and_check(sb, 0.8)
+
+
+def test_ragged_text_with_empty_and_long_samples():
+    sb = custom_stage(B=4, R=4, H=8, Hkv=8, d=128, T=[3, 200, 33, 129], N=[0, 70, 257, 5])
+    run_and_check(sb, 1.5)
+
+
+def test_lambda_zero_keeps_everything_and_huge_keeps_nothing():
+    sb = custom_stage(B=3, R=2, H=4, Hkv=2, d=64, T=[40] * 3, N=[100] * 3)
+    g, _ = run_and_check(sb, 0.0)
+    assert np.array_equal(g["kept_count"], sb.N)
+    g, _ = run_and_check(sb, 1e30)
+    assert np.all(g["kept_count"] == 0) and np.all(g["kept_offsets"] == 0)
+
+
+@pytest.mark.parametrize("reduce", [oracle.REG_MAX, oracle.REG_SUM])
+def test_other_register_reductions(reduce):
+    sb = custom_stage(B=2, R=8, H=8, Hkv=8, d=64, T=[1, 1], N=[500, 333])
+    run_and_check(sb, 0.9, reduce=reduce)
+
+
+def test_gqa_and_d72_text_rows():
+    sb = custom_stage(B=2, R=4, H=8, Hkv=2, d=72, T=[64, 17], N=[250, 90])
+    run_and_check(sb, 1.2)
+
+
+def test_f32_cls_d72_and_d256():
+    run_and_check(custom_stage(B=2, R=1, H=16, Hkv=16, d=72, T=[1, 1], N=[200, 31], dtype="f32"),
+                  1.0)
+    run_and_check(custom_stage(B=1, R=2, H=4, Hkv=1, d=256, T=[1], N=[100], dtype="f32"), 1.0)
+
+
+def test_text_path_at_one_row_matches_the_cls_path():
+    # A ragged problem whose rows are all 1 but whose row bound is 2 runs the MFMA path;
+    # the same problem with row bound 1 runs the VALU path.  Two independent codes, one
+    # answer.
+    sb = custom_stage(B=3, R=4, H=16, Hkv=16, d=64, T=[1, 1, 1], N=[576, 100, 31])
+    a = DeviceStage(sb, ragged=True)
+    a.prune(1.0)
+    ga = a.host()
+    b = DeviceStage(sb, ragged=True)
+    b.problem = occam.Problem(sb.B, sb.H, sb.Hkv, sb.d, sb.R, q_offsets=b.q_off,
+                              key_offsets=b.k_off, max_rows=2, max_cands=int(sb.N.max()),
+                              dtype=sb.dtype)
+    b.ws = occam.workspace(b.problem)
+    b.prune(1.0)
+    gb = b.host()
+    check_scores(gb["scores"], ga["scores"].astype(np.float64), 1e-4, "mfma vs valu")
+
+
+# ----------------------------------------------------------------------------- API variants
+def test_unfused_calls_equal_the_fused_call():
+    sb = synth.make_stage("llava15", "txt", B=3)
+    lam = lam_for("llava15", "txt")
+    ds = DeviceStage(sb)
+    ds.prune(lam)
+    fused = ds.host()
+    p, dev = ds.problem, "cuda"
+    scores = torch.empty(ds.total_keys, dtype=torch.float32, device=dev)
+    tau = torch.empty(sb.B, dtype=torch.float32, device=dev)
+    kept = torch.empty(ds.total_cands, dtype=torch.int32, device=dev)
+    cnt = torch.empty(sb.B, dtype=torch.int32, device=dev)
+    offs = torch.empty(sb.B + 1, dtype=torch.int32, device=dev)
+    occam.score(p, ds.q, ds.k, scores, ds.ws)
+    occam.threshold(p, scores, lam, occam.REG_MEAN, tau)
+    occam.select(p, scores, tau, kept, cnt, offs, ds.ws)
+    dsts = [torch.zeros_like(d) for d in ds.row_dst]
+    rows = [occam.Rows(s, d_, src_pad_rows=pl.pad_rows, src_row0=pl.row0)
+            for s, d_, pl in zip(ds.row_src, dsts, sb.payload)]
+    occam.gather(p, rows, kept, offs)
+    torch.cuda.synchronize()
+    total = int(offs[-1])
+    assert np.array_equal(scores.cpu().numpy(), fused["scores"])
+    assert np.array_equal(tau.cpu().numpy(), fused["tau"])
+    assert np.array_equal(kept[:total].cpu().numpy(), fused["kept_idx"])
+    assert np.array_equal(offs.cpu().numpy(), fused["kept_offsets"])
+    for d_, want in zip(dsts, fused["rows"]):
+        got = d_[:total].cpu()
+        got = got.view(torch.int16).numpy().view(np.uint16) if got.dtype == torch.bfloat16 else got.numpy()
+        assert np.array_equal(got.view(np.uint8), want.view(np.uint8))
+
+
+@pytest.mark.parametrize("name,stage", [("llava_next", "vis"), ("llava_next", "txt"),
+                                        ("qwen3vl_ragged", "txt")])
+def test_run_to_run_bitwise_determinism(name, stage):
+    sb = synth.make_stage(name, stage, B=4)
+    lam = lam_for(name, stage)
+    ds = DeviceStage(sb)
+    ds.prune(lam)
+    a = ds.host()
+    for v in ds.out.values():
+        v.fill_(-7)
+    ds.prune(lam)
+    b = ds.host()
+    for key in ("scores", "tau", "kept_idx", "kept_count", "kept_offsets"):
+        assert np.array_equal(a[key].view(np.uint8), b[key].view(np.uint8)), key
+
+
+def test_caller_normaliser_over_a_larger_key_set():
+    # row_lse from the caller (here: the log-sum-exp over the keys plus 24 extra keys that
+    # are not scored, computed on the host in float64) replaces the per-row softmax sum.
+    sb = custom_stage(B=2, R=4, H=8, Hkv=8, d=64, T=[20, 20], N=[150, 150], dtype="bf16")
+    rng = np.random.default_rng(5)
+    qf = synth.bf16_bits_to_f32(sb.q).reshape(-1, sb.H, sb.d).astype(np.float64)
+    kf = synth.bf16_bits_to_f32(sb.k).reshape(-1, sb.Hkv, sb.d).astype(np.float64)
+    scale = f32_scale(sb.d)
+    lse = np.empty((int(sb.q_off[-1]), sb.H))
+    for b in range(sb.B):
+        extra = rng.standard_normal((24, sb.Hkv, sb.d))
+        keys = np.concatenate([kf[sb.k_off[b]:sb.k_off[b + 1]], extra])
+        for t in range(sb.q_off[b], sb.q_off[b + 1]):
+            for h in range(sb.H):
+                lg = keys[:, h] @ qf[t, h] * scale
+                m = lg.max()
+                lse[t, h] = m + np.log(np.exp(lg - m).sum())
+    lse32 = lse.astype(np.float32)
+    ds = DeviceStage(sb)
+    ds.prune(0.7, row_lse=torch.from_numpy(lse32.reshape(-1)).cuda())
+    g = ds.host()
+    o = oracle_prune(sb, 0.7, row_lse=lse32.reshape(-1).astype(np.float64))
+    check_scores(g["scores"], o["scores"], RTOL["bf16"])
+    check_selection(g, o, sb, RTOL["bf16"])
+    check_rows(g, sb)
+
+
+def test_index_map_remaps_the_list_but_not_the_gather():
+    sb = custom_stage(B=3, R=2, H=4, Hkv=4, d=64, T=[9, 9, 9], N=[60, 0, 45])
+    rng = np.random.default_rng(8)
+    imap = rng.permutation(100000)[:int(sb.N.sum())].astype(np.int32)
+    ds = DeviceStage(sb, ragged=True)
+    ds.prune(1.1, index_map=torch.from_numpy(imap).cuda())
+    g = ds.host()
+    o = oracle_prune(sb, 1.1, index_map=imap)
+    check_scores(g["scores"], o["scores"], RTOL["bf16"])
+    check_selection(g, o, sb, RTOL["bf16"], index_map=imap)
+    # Rows are gathered at the local indices: recover them through the inverse map.
+    co = np.concatenate([[0], np.cumsum(sb.N)])
+    local = np.empty_like(g["kept_idx"])
+    for b in range(sb.B):
+        inv = {int(imap[co[b] + v]): v for v in range(sb.N[b])}
+        s, e = g["kept_offsets"][b], g["kept_offsets"][b + 1]
+        local[s:e] = [inv[int(x)] for x in g["kept_idx"][s:e]]
+    check_rows(dict(g, kept_idx=local), sb)
