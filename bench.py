@@ -77,6 +77,25 @@ def cpu_baseline(name, lam1, lam2, budget_s=15.0, max_samples=256):
                       "%.1f s" % (done, name, t_total)}
 
 
+def reference_lse(torch, txt, dt):
+    """Per-(row, head) natural log-sum-exp of a uniform text stage, float32 on the device.
+
+    Set-up for timing the scoring kernel alone (occam_score with a caller normaliser);
+    not part of any timed region.
+    """
+    B, S, T = txt.B, txt.R + int(txt.N[0]), int(txt.T[0])
+    lse = torch.empty(int(txt.q_off[-1]) * txt.H, dtype=torch.float32, device="cuda")
+    grp = txt.H // txt.Hkv
+    with torch.no_grad():
+        for b in range(B):
+            qh = dt.q[b * T:(b + 1) * T].float().permute(1, 0, 2).contiguous()      # [H, T, d]
+            kh = dt.k[b * S:(b + 1) * S].float().repeat_interleave(grp, dim=1)
+            kh = kh.permute(1, 2, 0).contiguous()                                    # [H, d, S]
+            lg = torch.matmul(qh, kh) / float(np.sqrt(np.float32(txt.d)))            # [H, T, S]
+            lse.view(-1, txt.H)[b * T:(b + 1) * T] = torch.logsumexp(lg, dim=-1).transpose(0, 1)
+    return lse
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -86,6 +105,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--kernel-reps", type=int, default=20,
                     help="timed repetitions of the dominant kernel alone")
+    ap.add_argument("--kernel-only", action="store_true",
+                    help="run only the dominant kernel (and a plain 1 GiB device copy of known "
+                         "size that calibrates byte counters), for counter collection")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the pruning path is per sample and needs no "
@@ -108,6 +130,23 @@ def main():
     lam2 = float(np.float32(lams["txt"]["lam"]))
 
     t0 = time.time()
+    if args.kernel_only:
+        txt = synth.make_stage(name, "txt", payload=False)
+        dt = DeviceStage(txt, ragged=txt.ragged, payload=False)
+        lse = reference_lse(torch, txt, dt)
+        scores_buf = torch.empty_like(dt.out["scores"])
+        for _ in range(args.kernel_reps):
+            occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws, row_lse=lse)
+        for _ in range(args.kernel_reps):
+            occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws)     # statistics + scoring
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        src.fill_(1)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log("kernel-only: %d launches of text_score alone, %d of text_stats + text_score, "
+            "one 1 GiB device copy" % (args.kernel_reps, args.kernel_reps))
+        return
     vis = synth.make_stage(name, "vis")
     txt = synth.make_stage(name, "txt")
     log("generated %s in %.1fs" % (name, time.time() - t0))
@@ -149,17 +188,7 @@ def main():
     # normaliser launches exactly that one kernel, so HIP events around the call on the
     # launch stream time it alone.  The normaliser is the true per-(row, head) log-sum-exp
     # (float32 matmul on the device; setup only).
-    lse = torch.empty(int(txt.q_off[-1]) * txt.H, dtype=torch.float32, device="cuda")
-    with torch.no_grad():
-        S = txt.R + int(txt.N[0])
-        T = int(txt.T[0])
-        grp = txt.H // txt.Hkv
-        for b in range(B):
-            qh = dt.q[b * T:(b + 1) * T].float().permute(1, 0, 2).contiguous()      # [H, T, d]
-            kh = dt.k[b * S:(b + 1) * S].float().repeat_interleave(grp, dim=1)
-            kh = kh.permute(1, 2, 0).contiguous()                                    # [H, d, S]
-            lg = torch.matmul(qh, kh) / float(np.sqrt(np.float32(txt.d)))            # [H, T, S]
-            lse.view(-1, txt.H)[b * T:(b + 1) * T] = torch.logsumexp(lg, dim=-1).transpose(0, 1)
+    lse = reference_lse(torch, txt, dt)
     scores_buf = torch.empty_like(dt.out["scores"])
     occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws, row_lse=lse)
     torch.cuda.synchronize()

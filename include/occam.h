@@ -59,6 +59,12 @@
  *
  * Precision.  Logits and probabilities are computed in float32 from float32
  * or bfloat16 inputs; bfloat16 products are exact in float32.
+ *
+ * Kernel coverage (anything else returns OCCAM_ERR_UNSUPPORTED):
+ *   one anchor row (rows == 1, or max_rows == 1): f32 or bf16, H <= 64, any d
+ *     that keeps a key head a whole number of 16-byte chunks, H*d small enough
+ *     for the query to sit in 64 KB of LDS with its partial sums;
+ *   several anchor rows: bf16 only (the MFMA path), d <= 128.
  */
 #ifndef OCCAM_H
 #define OCCAM_H

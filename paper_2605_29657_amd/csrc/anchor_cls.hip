@@ -21,6 +21,15 @@
 
 namespace occam {
 
+// exp for the softmax of the one-row path.  bfloat16 inputs are checked to 2e-2
+// relative, so the hardware exp2 (v_exp_f32 on x*log2(e), a few 1e-7 relative error
+// at the logit ranges seen here) suffices; float32 inputs are checked to 1e-5 and use
+// the device library's correctly rounded-to-1-ulp expf.
+template <bool BF16>
+__device__ __forceinline__ float cls_exp(float x) {
+    return BF16 ? __builtin_amdgcn_exp2f(x * kLog2e) : expf(x);
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(kClsThreads) void cls_logits_kernel(
     Prob p, const void* __restrict__ qv, const void* __restrict__ kv,
@@ -40,6 +49,7 @@ __global__ __launch_bounds__(kClsThreads) void cls_logits_kernel(
     int* tab = reinterpret_cast<int*>(qs + H * d);      // [CPK]: (g << 16) | part
     float* part = reinterpret_cast<float*>(tab + CPK);  // [nk][H][NC]
     float* lg = part + kpw * H * NC;                    // [nk][H]
+    float* red = lg + kpw * H;                          // [2 * blockDim]
 
     const int qrow = q_begin(p, b);
     if (BF16) {
@@ -99,44 +109,84 @@ __global__ __launch_bounds__(kClsThreads) void cls_logits_kernel(
     }
     __syncthreads();
 
-    for (int h = threadIdx.x; h < H; h += blockDim.x) {
-        float m = -INFINITY;
-        for (int key = 0; key < nk; ++key) m = fmaxf(m, lg[key * H + h]);
-        float z = 0.f;
-        for (int key = 0; key < nk; ++key) z += expf(lg[key * H + h] - m);
-        stats[((size_t)b * nchunks + c) * H + h] = make_float2(m, z);
+    // Per-head (max, sum exp) of this chunk: P threads per head, each over a strided
+    // subset of the chunk's keys, then a fixed-order merge of the P partials.
+    const int P = blockDim.x / H;                   // >= 1 (H <= 64)
+    const int hh = threadIdx.x % H, j0 = threadIdx.x / H;
+    float m = -INFINITY;
+    if (j0 < P)
+        for (int key = j0; key < nk; key += P) m = fmaxf(m, lg[key * H + hh]);
+    red[threadIdx.x] = m;
+    __syncthreads();
+    if (threadIdx.x < H) {
+        float mm = red[threadIdx.x];
+        for (int j = 1; j < P; ++j) mm = fmaxf(mm, red[j * H + threadIdx.x]);
+        red[blockDim.x + threadIdx.x] = mm;
+    }
+    __syncthreads();
+    const float mh = red[blockDim.x + hh];
+    float z = 0.f;
+    if (j0 < P)
+        for (int key = j0; key < nk; key += P) z += cls_exp<BF16>(lg[key * H + hh] - mh);
+    __syncthreads();
+    red[threadIdx.x] = z;
+    __syncthreads();
+    if (threadIdx.x < H) {
+        float zz = red[threadIdx.x];
+        for (int j = 1; j < P; ++j) zz += red[j * H + threadIdx.x];
+        stats[((size_t)b * nchunks + c) * H + threadIdx.x] = make_float2(mh, zz);
     }
 }
 
+template <bool BF16>
 __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
     Prob p, const float* __restrict__ logits, const float2* __restrict__ stats,
     const float* __restrict__ row_lse, float* __restrict__ scores, int kpw, int nchunks)
 {
-    extern __shared__ float smem[];
+    __shared__ float red_m[kClsThreads], red_z[kClsThreads];
+    __shared__ float mh[64], izh[64];
     const int c = blockIdx.x, b = blockIdx.y;
     const int S = keys_of(p, b);
     const int s0 = c * kpw;
     if (s0 >= S) return;
     const int nk = min(kpw, S - s0);
     const int H = p.H;
-    float* mh = smem;       // [H] per-head max (or the caller's log normaliser)
-    float* zh = smem + H;   // [H] per-head sum of exp(l - m)
     const int nch = (S + kpw - 1) / kpw;
-    for (int h = threadIdx.x; h < H; h += blockDim.x) {
-        if (row_lse) {
+    if (row_lse) {
+        for (int h = threadIdx.x; h < H; h += blockDim.x) {
             mh[h] = row_lse[(size_t)q_begin(p, b) * H + h];
-            zh[h] = 1.f;
-        } else {
-            const float2* st = stats + (size_t)b * nchunks * H + h;
-            float m = -INFINITY;
-            for (int j = 0; j < nch; ++j) m = fmaxf(m, st[(size_t)j * H].x);
-            float z = 0.f;
-            for (int j = 0; j < nch; ++j) {
+            izh[h] = 1.f;
+        }
+    } else {
+        // Merge the per-chunk (max, sum) pairs of the sample: P threads per head, each a
+        // strided subset of chunks, then a fixed-order merge of the P partials.
+        const int P = blockDim.x / H;
+        const int hh = threadIdx.x % H, j0 = threadIdx.x / H;
+        float m = -INFINITY, z = 0.f;
+        if (j0 < P) {
+            const float2* st = stats + (size_t)b * nchunks * H + hh;
+            for (int j = j0; j < nch; j += P) {
                 const float2 v = st[(size_t)j * H];
-                z += v.y * expf(v.x - m);
+                const float mn = fmaxf(m, v.x);
+                z = z * cls_exp<BF16>(m - mn) + v.y * cls_exp<BF16>(v.x - mn);
+                m = mn;
             }
-            mh[h] = m;
-            zh[h] = z;
+        }
+        red_m[threadIdx.x] = m;
+        red_z[threadIdx.x] = z;
+        __syncthreads();
+        if (threadIdx.x < H) {
+            float mm = red_m[threadIdx.x], zz = red_z[threadIdx.x];
+            for (int j = 1; j < P; ++j) {
+                const float mo = red_m[j * H + threadIdx.x], zo = red_z[j * H + threadIdx.x];
+                const float mn = fmaxf(mm, mo);
+                if (mn != -INFINITY) {
+                    zz = zz * cls_exp<BF16>(mm - mn) + zo * cls_exp<BF16>(mo - mn);
+                    mm = mn;
+                }
+            }
+            mh[threadIdx.x] = mm;
+            izh[threadIdx.x] = 1.f / zz;
         }
     }
     __syncthreads();
@@ -145,7 +195,7 @@ __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
     const float invH = 1.f / (float)H;
     for (int key = threadIdx.x; key < nk; key += blockDim.x) {
         float acc = 0.f;
-        for (int h = 0; h < H; ++h) acc += expf(lrow[key * H + h] - mh[h]) / zh[h];
+        for (int h = 0; h < H; ++h) acc += cls_exp<BF16>(lrow[key * H + h] - mh[h]) * izh[h];
         out[key] = acc * invH;
     }
 }
@@ -153,7 +203,7 @@ __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
 static size_t cls_logits_smem(const Prob& p, int bf16, int kpw) {
     const int NC = p.d / (bf16 ? 8 : 4);
     return sizeof(float) * ((size_t)p.H * p.d + (size_t)NC * p.Hkv + (size_t)kpw * p.H * NC +
-                            (size_t)kpw * p.H);
+                            (size_t)kpw * p.H + 2 * (size_t)kClsThreads);
 }
 
 hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void* k,
@@ -171,13 +221,17 @@ hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void*
     return hipGetLastError();
 }
 
-hipError_t launch_cls_scores(const Prob& p, const float* logits, const float2* stats,
+hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const float2* stats,
                              const float* row_lse, float* scores, int kpw, hipStream_t s)
 {
     const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
     dim3 grid(nchunks, p.B);
-    hipLaunchKernelGGL(cls_scores_kernel, grid, dim3(kClsThreads), 2 * p.H * sizeof(float), s, p,
-                       logits, stats, row_lse, scores, kpw, nchunks);
+    if (bf16)
+        hipLaunchKernelGGL(cls_scores_kernel<true>, grid, dim3(kClsThreads), 0, s, p, logits, stats,
+                           row_lse, scores, kpw, nchunks);
+    else
+        hipLaunchKernelGGL(cls_scores_kernel<false>, grid, dim3(kClsThreads), 0, s, p, logits,
+                           stats, row_lse, scores, kpw, nchunks);
     return hipGetLastError();
 }
 

@@ -56,13 +56,56 @@ __device__ __forceinline__ void merge_pair(float& m, float& z, float mo, float z
     m = mn;
 }
 
-template <int DS>
-__global__ __launch_bounds__(kTxtThreads) void text_stats_kernel(
+// Loads are unconditional so that the compiler can count outstanding loads and
+// keep prefetches in flight: key and row indices are clamped into range (a
+// clamped key's logits are never used, a clamped row's results are never
+// written or carry zero weight), and when d % 16 == 8 (HALF) the upper lane
+// half of the last 16-wide step reads a valid address and is zeroed by select.
+template <int DS, bool HALF>
+__device__ __forceinline__ u32x4 frag16(const uint16_t* row, int kk, int hi) {
+    const bool pad = HALF && kk == DS - 1 && hi;
+    u32x4 v = load16(row + kk * 16 + (pad ? 0 : hi * 8));
+    const u32x4 zero = {0u, 0u, 0u, 0u};
+    return pad ? zero : v;
+}
+
+// Copy 16 bytes per lane straight from global memory into LDS (gfx950
+// global_load_lds_dwordx4): lane l of the wave writes lds_base + 16 l.
+__device__ __forceinline__ void dma16(const void* gsrc, void* lds_base) {
+    __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+}
+// Wait until every global load of this wave (including LDS copies) has landed.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// vmcnt(n) wait with expcnt / lgkmcnt left unconstrained (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmem_le() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
+}
+
+template <int DS, bool HALF>
+__global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     float* __restrict__ lse2)
 {
-    __shared__ float red_m[kTxtThreads / kWave][kTxtRows];
-    __shared__ float red_z[kTxtThreads / kWave][kTxtRows];
+    // 8 waves: wave w owns rows [64*(w&1), +64) of the row block and the key stream
+    // ks = w>>1 (key blocks kbi = ks (mod 4)).  The two waves of a stream consume the
+    // same key blocks, so each block is copied once per pair, global -> LDS, into a
+    // ring of kRing stages per stream: kRing - 1 blocks are in flight while one is
+    // used.  A block is 32 keys x NCH 16-byte chunks; LDS unit key*NCH + j holds
+    // chunk (j + key) % NCH of that key (a rotation), so the MFMA fragment reads of
+    // 32 consecutive keys spread over the banks.
+    constexpr int kStreams = kStatsThreads / kWave / 2;
+    constexpr int NCH = 2 * DS;                      // 16-byte chunks per key row
+    constexpr int UNITS = 32 * NCH;                  // 16-byte units per block
+    constexpr int COPIES = UNITS / kWave;            // = DS copies of 64 lanes per block
+    constexpr int MINE0 = (COPIES + 1) / 2, MINE1 = COPIES / 2;   // copies per pair member
+    extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+    u32x4* ring = reinterpret_cast<u32x4*>(smem_raw);              // [stream][stage][UNITS]
+    float* red_m = reinterpret_cast<float*>(ring + kStreams * kStatsRing * UNITS);
+    float* red_z = red_m + kStreams * kTxtRows;
+
     const int tblk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int T = rows_of(p, b);
     const int t0 = tblk * kTxtRows;
@@ -70,115 +113,159 @@ __global__ __launch_bounds__(kTxtThreads) void text_stats_kernel(
     const int S = keys_of(p, b);
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int hi = lane >> 5, lo = lane & 31;
+    const int rh = wave & 1, ks = wave >> 1;
     const int H = p.H, Hkv = p.Hkv, d = p.d;
     const int g = h / (H / Hkv);
-    const int nsb = min(4, (T - t0 + 31) >> 5);
+    const int tw = t0 + rh * 64;                       // first row of this wave
+    const int nsb = max(0, min(2, (T - tw + 31) >> 5));
     const int qb = q_begin(p, b), kb0 = k_begin(p, b);
     const float c2 = p.scale * kLog2e;
 
-    bf16x8 qf[4][DS];
+    bf16x8 qf[2][DS];
 #pragma unroll
-    for (int sb = 0; sb < 4; ++sb) {
-        const int t = t0 + sb * 32 + lo;
+    for (int sb = 0; sb < 2; ++sb) {
+        const int t = min(tw + sb * 32 + lo, T - 1);
+        const uint16_t* qrow = q + ((size_t)(qb + t) * H + h) * d;
 #pragma unroll
-        for (int kk = 0; kk < DS; ++kk) {
-            const int e = kk * 16 + hi * 8;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (t < T && e < d) v = load16(q + ((size_t)(qb + t) * H + h) * d + e);
-            qf[sb][kk] = as_bf16x8(v);
-        }
+        for (int kk = 0; kk < DS; ++kk) qf[sb][kk] = as_bf16x8(frag16<DS, HALF>(qrow, kk, hi));
     }
 
-    float m[4], z[4];
+    float m[2], z[2];
 #pragma unroll
-    for (int sb = 0; sb < 4; ++sb) { m[sb] = -INFINITY; z[sb] = 0.f; }
+    for (int sb = 0; sb < 2; ++sb) { m[sb] = -INFINITY; z[sb] = 0.f; }
 
     const int nkb = (S + 31) >> 5;
+    const int nmine = (nkb - ks + kStreams - 1) / kStreams;     // blocks of this stream
     const uint16_t* kbase = k + ((size_t)kb0 * Hkv + g) * d;
     const size_t kstride = (size_t)Hkv * d;
-    auto load_k = [&](int kbi, u32x4 (&kf)[DS]) {
-        const int key = kbi * 32 + lo;
+    u32x4* sring = ring + ks * kStatsRing * UNITS;
+
+    // Copy block j of this stream (clamped to the stream's last block) into its stage.
+    // Copy c of the block covers units 64c .. 64c+63; this wave issues c = rh, rh+2, ...
+    // Chunks past d (HALF) read chunk 0 of the key: their fragment is zeroed below.
+    auto issue = [&](int j) {
+        const int jj = min(j, max(nmine - 1, 0));
+        const int kbi = ks + jj * kStreams;
+        u32x4* dst = sring + (jj % kStatsRing) * UNITS;
 #pragma unroll
-        for (int kk = 0; kk < DS; ++kk) {
-            const int e = kk * 16 + hi * 8;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (key < S && e < d) v = load16(kbase + (size_t)key * kstride + e);
-            kf[kk] = v;
+        for (int c = rh; c < COPIES; c += 2) {
+            const int u = c * kWave + lane;
+            const int key = u / NCH, pos = u % NCH;
+            const int ch = (pos + key) % NCH;
+            const int kg = min(kbi * 32 + key, S - 1);
+            const int e = (HALF && ch == NCH - 1) ? 0 : ch * 8;
+            dma16(kbase + (size_t)kg * kstride + e, dst + c * kWave);
         }
     };
 
-    u32x4 kcur[DS], knext[DS];
-    int kbi = wave;
-    if (kbi < nkb) load_k(kbi, kcur);
-    for (; kbi < nkb; kbi += 4) {
-        if (kbi + 4 < nkb) load_k(kbi + 4, knext);
+    // One key block: MFMA logits from the LDS stage, then the online (max, sum) update.
+    auto block = [&](int kbi, const u32x4* blk) {
         const int nvalid = S - kbi * 32;
+        u32x4 kf[DS];
 #pragma unroll
-        for (int sb = 0; sb < 4; ++sb) {
+        for (int kk = 0; kk < DS; ++kk) {
+            const int ch = 2 * kk + hi;
+            const u32x4 v = blk[lo * NCH + (ch - lo % NCH + NCH) % NCH];
+            const u32x4 zero = {0u, 0u, 0u, 0u};
+            kf[kk] = (HALF && kk == DS - 1 && hi) ? zero : v;
+        }
+        f32x16 acc[2];
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb) acc[sb] = f32x16{};
+#pragma unroll
+        for (int kk = 0; kk < DS; ++kk) {
+            acc[0] = mfma32(as_bf16x8(kf[kk]), qf[0][kk], acc[0]);
+            if (nsb > 1) acc[1] = mfma32(as_bf16x8(kf[kk]), qf[1][kk], acc[1]);
+        }
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb) {
             if (sb >= nsb) break;
-            f32x16 acc = {};
-#pragma unroll
-            for (int kk = 0; kk < DS; ++kk) acc = mfma32(as_bf16x8(kcur[kk]), qf[sb][kk], acc);
             float mx = -INFINITY;
             if (nvalid >= 32) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[r]);
+                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[sb][r]);
             } else {
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    if (acc_key(r, hi) < nvalid) mx = fmaxf(mx, acc[r]);
+                    if (acc_key(r, hi) < nvalid) mx = fmaxf(mx, acc[sb][r]);
             }
             if (mx == -INFINITY) continue;
             const float mn = fmaxf(m[sb], mx * c2);
             float sum = 0.f;
             if (nvalid >= 32) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(fmaf(acc[r], c2, -mn));
+                for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -mn));
             } else {
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    if (acc_key(r, hi) < nvalid) sum += __builtin_amdgcn_exp2f(fmaf(acc[r], c2, -mn));
+                    if (acc_key(r, hi) < nvalid) sum += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -mn));
             }
             z[sb] = z[sb] * __builtin_amdgcn_exp2f(m[sb] - mn) + sum;
             m[sb] = mn;
         }
-#pragma unroll
-        for (int kk = 0; kk < DS; ++kk) kcur[kk] = knext[kk];
-    }
+    };
 
-    // Merge the two lane halves (same rows, different keys), then the waves.
+    // Every wave runs the same number of iterations (the most any stream has), so the
+    // barriers match; a stream past its last block only re-issues its last block.
+    const int iters = (nkb + kStreams - 1) / kStreams;
 #pragma unroll
-    for (int sb = 0; sb < 4; ++sb) {
+    for (int j = 0; j < kStatsRing - 1; ++j) issue(j);
+    for (int i = 0; i < iters; ++i) {
+        // Own copies of block i have landed once at most kStatsRing-2 later blocks remain.
+        if (rh == 0) wait_vmem_le<(kStatsRing - 2) * MINE0>();
+        else wait_vmem_le<(kStatsRing - 2) * MINE1>();
+        __syncthreads();                 // partner's copies landed; stage (i-1) is free
+        issue(i + kStatsRing - 1);
+        if (i < nmine && nsb > 0) block(ks + i * kStreams, sring + (i % kStatsRing) * UNITS);
+    }
+    wait_vmem_le<0>();
+
+    // Merge the two lane halves (same rows, different keys), then the key streams.
+#pragma unroll
+    for (int sb = 0; sb < 2; ++sb) {
         const float mo = __shfl_xor(m[sb], 32);
         const float zo = __shfl_xor(z[sb], 32);
         merge_pair(m[sb], z[sb], mo, zo);
         if (hi == 0) {
-            red_m[wave][sb * 32 + lo] = m[sb];
-            red_z[wave][sb * 32 + lo] = z[sb];
+            red_m[ks * kTxtRows + rh * 64 + sb * 32 + lo] = m[sb];
+            red_z[ks * kTxtRows + rh * 64 + sb * 32 + lo] = z[sb];
         }
     }
     __syncthreads();
     if (threadIdx.x < kTxtRows) {
         const int i = threadIdx.x;
-        float mm = red_m[0][i], zz = red_z[0][i];
-        for (int w = 1; w < kTxtThreads / kWave; ++w) merge_pair(mm, zz, red_m[w][i], red_z[w][i]);
+        float mm = red_m[i], zz = red_z[i];
+        for (int w = 1; w < kStreams; ++w) merge_pair(mm, zz, red_m[w * kTxtRows + i], red_z[w * kTxtRows + i]);
         const int t = t0 + i;
         if (t < T) lse2[(size_t)(qb + t) * H + h] = mm + __builtin_amdgcn_logf(zz);
     }
 }
 
-template <int DS>
-__global__ __launch_bounds__(kTxtThreads) void text_score_kernel(
+template <int DS, bool HALF, bool MULTI>
+__global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const float* __restrict__ lse, int lse_natural, float* __restrict__ scores)
 {
-    constexpr int DP = DS * 16 + 8;             // padded LDS row (elements)
-    constexpr int QCH = kTxtRows * DS * 2 / kTxtThreads;  // 16-byte Q chunks per thread
+    // 4 waves: wave w owns the 32 keys [s_lo + 32 w, +32) and all 128 rows of the
+    // current row block (4 sub-blocks of 32 rows, computed as two interleaved MFMA
+    // accumulator chains).  Two workgroups share a CU, so one workgroup's MFMAs
+    // overlap the other's exponentials.
+    //
+    // The query tile of a head lives in LDS chunk-major, qt[c][row] (16-byte units,
+    // c = 8-element chunk of d), double-buffered: the next head's tile is copied
+    // global -> LDS directly while the current head is computed, so the copy needs
+    // no registers and each head needs one barrier.  Reading fragment (row, c) for
+    // 32 consecutive rows touches 32 consecutive 16-byte units: no bank conflicts.
+    constexpr int NCH = 2 * DS;                                   // 16-byte chunks per row
+    constexpr int QTILE = kTxtRows * NCH;                         // 16-byte units per tile
+    constexpr int COPIES = QTILE / kWave / (kScoreThreads / kWave);  // per wave per tile
     extern __shared__ __attribute__((aligned(16))) char smem_raw[];
-    uint16_t* qt = reinterpret_cast<uint16_t*>(smem_raw);                 // [128][DP]
-    float* l2t = reinterpret_cast<float*>(smem_raw + kTxtRows * DP * 2);  // [H][128]
+    u32x4* qt = reinterpret_cast<u32x4*>(smem_raw);                         // [2][NCH][128]
+    float* l2t = reinterpret_cast<float*>(smem_raw + 2 * QTILE * 16);       // [H][128]
 
-    const int c = blockIdx.x, b = blockIdx.y;
+    // Samples in reverse order: the statistics pass streamed sample B-1 last, so its
+    // keys are the likeliest to still sit in the memory-side cache.
+    const int c = blockIdx.x, b = p.B - 1 - (int)blockIdx.y;
     const int S = keys_of(p, b);
     const int s_lo = c * kTxtKeysPerWg;
     if (s_lo >= S) return;
@@ -192,44 +279,41 @@ __global__ __launch_bounds__(kTxtThreads) void text_score_kernel(
     const bool wactive = wkey0 < S;
     const int R = p.R;
 
-    auto load_q = [&](int hh, int t0, u32x4 (&qr)[QCH]) {
+    // Copy head hh's query tile (rows t0..t0+127) into buffer buf.  Copy j of this
+    // wave covers chunk c = u / 2 and rows 64 (u % 2) .. +64 with u = wave*COPIES + j.
+    // Rows past T_b are clamped (their lse2 is +inf, so they weigh exactly 0); the pad
+    // chunk past d (HALF) reads chunk 0 instead, harmless because the matching key
+    // chunk is zero.
+    auto copy_q = [&](int hh, int t0, int buf) {
+        hh = min(hh, H - 1);
 #pragma unroll
-        for (int j = 0; j < QCH; ++j) {
-            const int i = tid + j * kTxtThreads;
-            const int row = i / (DS * 2), e = (i % (DS * 2)) * 8;
-            const int t = t0 + row;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (t < T && e < d) v = load16(q + ((size_t)(qb + t) * H + hh) * d + e);
-            qr[j] = v;
+        for (int j = 0; j < COPIES; ++j) {
+            const int u = wave * COPIES + j;
+            const int ch = u >> 1, r0 = (u & 1) * 64;
+            const int t = min(t0 + r0 + lane, T - 1);
+            const int e = (HALF && ch == NCH - 1) ? 0 : ch * 8;
+            dma16(q + ((size_t)(qb + t) * H + hh) * d + e, qt + (buf * NCH + ch) * kTxtRows + r0);
         }
     };
-    auto store_q = [&](const u32x4 (&qr)[QCH]) {
+    const int kclamp = min(wkey0 + lo, S - 1);        // keys past S_b are never written
+    auto load_k = [&](int hh, u32x4 (&kf)[DS]) {
+        const int gg = min(hh, H - 1) / group;
+        const uint16_t* krow = k + ((size_t)(kb0 + kclamp) * Hkv + gg) * d;
 #pragma unroll
-        for (int j = 0; j < QCH; ++j) {
-            const int i = tid + j * kTxtThreads;
-            const int row = i / (DS * 2), e = (i % (DS * 2)) * 8;
-            *reinterpret_cast<u32x4*>(qt + row * DP + e) = qr[j];
-        }
-    };
-    auto load_k = [&](int gg, u32x4 (&kf)[DS]) {
-        const int key = wkey0 + lo;
-#pragma unroll
-        for (int kk = 0; kk < DS; ++kk) {
-            const int e = kk * 16 + hi * 8;
-            u32x4 v = {0u, 0u, 0u, 0u};
-            if (key < S && e < d) v = load16(k + ((size_t)(kb0 + key) * Hkv + gg) * d + e);
-            kf[kk] = v;
-        }
+        for (int kk = 0; kk < DS; ++kk) kf[kk] = frag16<DS, HALF>(krow, kk, hi);
     };
 
-    float vmax[16], rsum[16];
+    float vmax[MULTI ? 16 : 1], rsum[MULTI ? 16 : 1];
+    if (MULTI) {
 #pragma unroll
-    for (int r = 0; r < 16; ++r) { vmax[r] = 0.f; rsum[r] = 0.f; }
+        for (int r = 0; r < 16; ++r) { vmax[r] = 0.f; rsum[r] = 0.f; }
+    }
+    float abar[4][16];
 
     for (int t0 = 0; t0 < T; t0 += kTxtRows) {
         const int nsb = min(4, (T - t0 + 31) >> 5);
         __syncthreads();  // previous row block is done with qt / l2t
-        for (int i = tid; i < H * kTxtRows; i += kTxtThreads) {
+        for (int i = tid; i < H * kTxtRows; i += kScoreThreads) {
             const int hh = i / kTxtRows, t = t0 + (i % kTxtRows);
             float v = INFINITY;
             if (t < T) {
@@ -238,66 +322,84 @@ __global__ __launch_bounds__(kTxtThreads) void text_score_kernel(
             }
             l2t[i] = v;
         }
-        u32x4 qreg[QCH];
-        u32x4 kcur[DS], knext[DS];
-        load_q(0, t0, qreg);
-        if (wactive) load_k(0, kcur);
-        store_q(qreg);
-        if (H > 1) load_q(1, t0, qreg);
+        u32x4 k0[DS], k1[DS];
+        copy_q(0, t0, 0);
+        load_k(0, k0);
+        wait_vmem();
         __syncthreads();
 
-        float abar[4][16];
 #pragma unroll
         for (int sb = 0; sb < 4; ++sb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) abar[sb][r] = 0.f;
 
-        for (int h = 0; h < H; ++h) {
+        // One head: start the copies of head h+1 (query tile to the other buffer, key
+        // fragments to registers), MFMA logits of the wave's 32 keys x 128 rows (two
+        // accumulator chains at a time), p = 2^(x - lse2), head sum; then wait for the
+        // copies and synchronise.
+        auto head = [&](int h, const u32x4 (&kf)[DS], u32x4 (&kn)[DS]) {
+            const int buf = h & 1;
+            copy_q(h + 1, t0, buf ^ 1);
+            load_k(h + 1, kn);
             if (wactive) {
-                if (h + 1 < H) load_k((h + 1) / group, knext);
+                const u32x4* qb_ = qt + buf * NCH * kTxtRows;
 #pragma unroll
-                for (int sb = 0; sb < 4; ++sb) {
-                    if (sb >= nsb) break;
-                    f32x16 acc = {};
+                for (int sp = 0; sp < 4; sp += 2) {
+                    if (sp >= nsb) break;
+                    const int row0 = sp * 32 + lo, row1 = row0 + 32;
+                    f32x16 acc0 = {}, acc1 = {};
 #pragma unroll
                     for (int kk = 0; kk < DS; ++kk) {
-                        const u32x4 qv = *reinterpret_cast<const u32x4*>(
-                            qt + (sb * 32 + lo) * DP + kk * 16 + hi * 8);
-                        acc = mfma32(as_bf16x8(kcur[kk]), as_bf16x8(qv), acc);
+                        const int ch = 2 * kk + hi;
+                        const u32x4 q0 = qb_[ch * kTxtRows + row0];
+                        const u32x4 q1 = qb_[ch * kTxtRows + row1];
+                        acc0 = mfma32(as_bf16x8(kf[kk]), as_bf16x8(q0), acc0);
+                        acc1 = mfma32(as_bf16x8(kf[kk]), as_bf16x8(q1), acc1);
                     }
-                    const float l2 = l2t[h * kTxtRows + sb * 32 + lo];
+                    const float l20 = l2t[h * kTxtRows + row0];
+                    const float l21 = l2t[h * kTxtRows + row1];
 #pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        abar[sb][r] += __builtin_amdgcn_exp2f(fmaf(acc[r], c2, -l2));
+                    for (int r = 0; r < 16; ++r) {
+                        abar[sp][r] += __builtin_amdgcn_exp2f(fmaf(acc0[r], c2, -l20));
+                        abar[sp + 1][r] += __builtin_amdgcn_exp2f(fmaf(acc1[r], c2, -l21));
+                    }
                 }
-#pragma unroll
-                for (int kk = 0; kk < DS; ++kk) kcur[kk] = knext[kk];
             }
-            __syncthreads();  // every wave is done reading head h's tile
-            if (h + 1 < H) {
-                store_q(qreg);
-                if (h + 2 < H) load_q(h + 2, t0, qreg);
-            }
+            wait_vmem();
             __syncthreads();
+        };
+        for (int h = 0; h < H; h += 2) {
+            head(h, k0, k1);
+            if (h + 1 >= H) break;
+            head(h + 1, k1, k0);
         }
-#pragma unroll
-        for (int sb = 0; sb < 4; ++sb) {
-            if (sb >= nsb) break;
+        if (MULTI) {
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-                vmax[r] = fmaxf(vmax[r], abar[sb][r]);
-                rsum[r] += abar[sb][r];
+                vmax[r] = fmaxf(vmax[r], fmaxf(fmaxf(abar[0][r], abar[1][r]),
+                                               fmaxf(abar[2][r], abar[3][r])));
+                rsum[r] += (abar[0][r] + abar[1][r]) + (abar[2][r] + abar[3][r]);
             }
         }
     }
 
-    // Row reduction across the 32 lanes that share a lane half (fixed order).
+    // Row reduction of Eq. text_scoring: over the lane's sub-blocks, then across the 32
+    // lanes of a lane half (fixed order).  Rows past T_b hold exact zeros.
+    const bool regs = wactive && wkey0 < R;           // only the first key block has registers
+    float mx[16], sm[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
+        if (MULTI) {
+            mx[r] = vmax[r];
+            sm[r] = rsum[r];
+        } else {
+            mx[r] = fmaxf(fmaxf(abar[0][r], abar[1][r]), fmaxf(abar[2][r], abar[3][r]));
+            sm[r] = (abar[0][r] + abar[1][r]) + (abar[2][r] + abar[3][r]);
+        }
 #pragma unroll
         for (int off = 16; off >= 1; off >>= 1) {
-            vmax[r] = fmaxf(vmax[r], __shfl_xor(vmax[r], off));
-            rsum[r] += __shfl_xor(rsum[r], off);
+            mx[r] = fmaxf(mx[r], __shfl_xor(mx[r], off));
+            if (regs) sm[r] += __shfl_xor(sm[r], off);
         }
     }
     if (wactive && lo == 0) {
@@ -306,57 +408,69 @@ __global__ __launch_bounds__(kTxtThreads) void text_score_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int key = wkey0 + acc_key(r, hi);
-            if (key < S) scores[kb0 + key] = key < R ? rsum[r] * invHT : vmax[r] * invH;
+            if (key < S) scores[kb0 + key] = key < R ? sm[r] * invHT : mx[r] * invH;
         }
     }
 }
 
-template <int DS>
+template <int DS, bool HALF>
 static hipError_t stats_ds(const Prob& p, const void* q, const void* k, float* lse2, hipStream_t s) {
+    const size_t smem = text_stats_smem(DS * 16);
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&text_stats_kernel<DS, HALF>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kScoreSmemMax);
+    if (attr != hipSuccess) return attr;
     dim3 grid((p.max_rows + kTxtRows - 1) / kTxtRows, p.H, p.B);
-    hipLaunchKernelGGL(text_stats_kernel<DS>, grid, dim3(kTxtThreads), 0, s, p,
+    hipLaunchKernelGGL((text_stats_kernel<DS, HALF>), grid, dim3(kStatsThreads), smem, s, p,
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse2);
     return hipGetLastError();
 }
 
-template <int DS>
-static hipError_t score_ds(const Prob& p, const void* q, const void* k, const float* lse,
-                           int lse_natural, float* scores, hipStream_t s) {
+template <int DS, bool HALF, bool MULTI>
+static hipError_t score_launch(const Prob& p, const void* q, const void* k, const float* lse,
+                               int lse_natural, float* scores, hipStream_t s) {
+    const size_t smem = text_score_smem(p.H, DS * 16);
+    // The tile needs more than the default 64 KB of dynamic LDS: raise the limit once.
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&text_score_kernel<DS, HALF, MULTI>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kScoreSmemMax);
+    if (attr != hipSuccess) return attr;
     dim3 grid((p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg, p.B);
-    const size_t smem = (size_t)kTxtRows * (DS * 16 + 8) * 2 + (size_t)p.H * kTxtRows * 4;
-    hipLaunchKernelGGL(text_score_kernel<DS>, grid, dim3(kTxtThreads), smem, s, p,
+    hipLaunchKernelGGL((text_score_kernel<DS, HALF, MULTI>), grid, dim3(kScoreThreads), smem, s, p,
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
                        lse_natural, scores);
     return hipGetLastError();
 }
 
+template <int DS, bool HALF>
+static hipError_t score_ds(const Prob& p, const void* q, const void* k, const float* lse,
+                           int lse_natural, float* scores, hipStream_t s) {
+    if (p.max_rows > kTxtRows) return score_launch<DS, HALF, true>(p, q, k, lse, lse_natural, scores, s);
+    return score_launch<DS, HALF, false>(p, q, k, lse, lse_natural, scores, s);
+}
+
+// d = 16*DS (HALF = false) or 16*DS - 8 (HALF = true), d <= 128.
+#define OCCAM_D_SWITCH(FN, ...)                                                  \
+    switch (p.d) {                                                               \
+        case 8: return FN<1, true>(__VA_ARGS__);    case 16: return FN<1, false>(__VA_ARGS__);  \
+        case 24: return FN<2, true>(__VA_ARGS__);   case 32: return FN<2, false>(__VA_ARGS__);  \
+        case 40: return FN<3, true>(__VA_ARGS__);   case 48: return FN<3, false>(__VA_ARGS__);  \
+        case 56: return FN<4, true>(__VA_ARGS__);   case 64: return FN<4, false>(__VA_ARGS__);  \
+        case 72: return FN<5, true>(__VA_ARGS__);   case 80: return FN<5, false>(__VA_ARGS__);  \
+        case 88: return FN<6, true>(__VA_ARGS__);   case 96: return FN<6, false>(__VA_ARGS__);  \
+        case 104: return FN<7, true>(__VA_ARGS__);  case 112: return FN<7, false>(__VA_ARGS__); \
+        case 120: return FN<8, true>(__VA_ARGS__);  case 128: return FN<8, false>(__VA_ARGS__); \
+        default: return hipErrorInvalidValue;                                    \
+    }
 
 hipError_t launch_text_stats(const Prob& p, const void* q, const void* k, float* lse2,
                              hipStream_t s) {
-    const int ds = (p.d + 15) / 16;
-#define OCCAM_STATS(DSV) stats_ds<DSV>(p, q, k, lse2, s)
-    switch (ds) {
-        case 1: return OCCAM_STATS(1); case 2: return OCCAM_STATS(2);
-        case 3: return OCCAM_STATS(3); case 4: return OCCAM_STATS(4);
-        case 5: return OCCAM_STATS(5); case 6: return OCCAM_STATS(6);
-        case 7: return OCCAM_STATS(7); case 8: return OCCAM_STATS(8);
-        default: return hipErrorInvalidValue;
-    }
-#undef OCCAM_STATS
+    OCCAM_D_SWITCH(stats_ds, p, q, k, lse2, s)
 }
 
 hipError_t launch_text_score(const Prob& p, const void* q, const void* k, const float* lse,
                              int lse_natural, float* scores, hipStream_t s) {
-    const int ds = (p.d + 15) / 16;
-#define OCCAM_SCORE(DSV) score_ds<DSV>(p, q, k, lse, lse_natural, scores, s)
-    switch (ds) {
-        case 1: return OCCAM_SCORE(1); case 2: return OCCAM_SCORE(2);
-        case 3: return OCCAM_SCORE(3); case 4: return OCCAM_SCORE(4);
-        case 5: return OCCAM_SCORE(5); case 6: return OCCAM_SCORE(6);
-        case 7: return OCCAM_SCORE(7); case 8: return OCCAM_SCORE(8);
-        default: return hipErrorInvalidValue;
-    }
-#undef OCCAM_SCORE
+    OCCAM_D_SWITCH(score_ds, p, q, k, lse, lse_natural, scores, s)
 }
 
 }  // namespace occam

@@ -59,15 +59,15 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
     size_t off = 0;
     if (P.text) {
         if (!bf16 || d > 128) return OCCAM_ERR_UNSUPPORTED;
-        const size_t smem = (size_t)kTxtRows * (((d + 15) / 16) * 16 + 8) * 2 + (size_t)H * kTxtRows * 4;
-        if (smem > 65536) return OCCAM_ERR_UNSUPPORTED;
+        if (text_score_smem(H, ((d + 15) / 16) * 16) > kScoreSmemMax) return OCCAM_ERR_UNSUPPORTED;
         P.off_lse2 = off; off = align_up(off + (size_t)rows_cap * H * sizeof(float));
     } else {
         P.kpw = cls_keys_per_wg(H, d, bf16 ? 2 : 4);
         const int NC = d / (bf16 ? 8 : 4);
         const size_t smem = sizeof(float) * ((size_t)H * d + (size_t)NC * x.num_kv_heads +
-                                             (size_t)P.kpw * H * NC + (size_t)P.kpw * H);
-        if (smem > 65536) return OCCAM_ERR_UNSUPPORTED;
+                                             (size_t)P.kpw * H * NC + (size_t)P.kpw * H +
+                                             2 * (size_t)kClsThreads);
+        if (smem > 65536 || H > 64) return OCCAM_ERR_UNSUPPORTED;
         const long long nchunks = (R + (long long)max_cands + P.kpw - 1) / P.kpw;
         P.off_logits = off; off = align_up(off + (size_t)keys_cap * H * sizeof(float));
         P.off_stats = off; off = align_up(off + (size_t)B * nchunks * H * sizeof(float2));
@@ -138,7 +138,7 @@ occam_status run_score(const Plan& P, const void* q, const void* k, const float*
     float2* stats = ws_at<float2>(ws, P.off_stats);
     occam_status st = hip_ok(launch_cls_logits(P.p, P.bf16, q, k, logits, stats, P.kpw, s));
     if (st != OCCAM_OK) return st;
-    return hip_ok(launch_cls_scores(P.p, logits, stats, row_lse, scores, P.kpw, s));
+    return hip_ok(launch_cls_scores(P.p, P.bf16, logits, stats, row_lse, scores, P.kpw, s));
 }
 
 }  // namespace

@@ -72,11 +72,28 @@ constexpr int kClsPartials = 8192;   // LDS floats of per-chunk partial dot prod
 // Text (T > 1) path: MFMA 32x32x16 bf16; 4 waves; a t-block of 128 anchor rows
 // (4 sub-blocks of 32) and 32 keys per wave.
 constexpr int kTxtThreads = 256;
+constexpr int kStatsThreads = 512;
+constexpr int kScoreThreads = 256;
 constexpr int kTxtRows = 128;
 constexpr int kTxtKeysPerWave = 32;
-constexpr int kTxtKeysPerWg = kTxtKeysPerWave * (kTxtThreads / kWave);
+constexpr int kTxtKeysPerWg = 128;   // score kernel: 4 key blocks of 32
 constexpr int kSelThreads = 256;
 constexpr int kGatherThreads = 256;
+
+// Dynamic LDS of the text-row scoring kernel: two query tiles (128 rows x d bf16)
+// and the [H][128] float normaliser tile; at most kScoreSmemMax.
+constexpr size_t kScoreSmemMax = 160 * 1024;
+inline size_t text_score_smem(int H, int d16) {
+    return 2 * (size_t)kTxtRows * d16 * 2 + (size_t)H * kTxtRows * 4;
+}
+
+// Dynamic LDS of the text-row statistics kernel: a ring of kStatsRing key blocks
+// (32 keys x d bf16) per key stream, plus the (max, sum) merge arrays.
+constexpr int kStatsRing = 4;
+inline size_t text_stats_smem(int d16) {
+    return (size_t)(kStatsThreads / kWave / 2) * kStatsRing * 32 * d16 * 2 +
+           2 * (size_t)(kStatsThreads / kWave / 2) * kTxtRows * 4;
+}
 
 // Anchor-path keys per workgroup for a given row geometry.
 inline int cls_keys_per_wg(int H, int d, int elem_bytes) {
@@ -91,7 +108,7 @@ inline int cls_keys_per_wg(int H, int d, int elem_bytes) {
 // Launchers (defined in the .hip files).  All return hipGetLastError().
 hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void* k,
                              float* logits, float2* stats, int kpw, hipStream_t s);
-hipError_t launch_cls_scores(const Prob& p, const float* logits, const float2* stats,
+hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const float2* stats,
                              const float* row_lse, float* scores, int kpw, hipStream_t s);
 hipError_t launch_text_stats(const Prob& p, const void* q, const void* k, float* lse2,
                              hipStream_t s);

@@ -4,11 +4,12 @@
 // dense copy of their rows that forms the pruned sequence of Algorithm 1.
 //
 // threshold    one thread per sample: tau = lambda * reduce(register scores).
-// select       one workgroup per sample: each 256-candidate step evaluates the
-//              test, takes a wave ballot, ranks lanes with mbcnt and the
-//              waves with a 4-entry LDS scan, and appends the survivors'
-//              candidate-local indices, ascending, to the sample's slot of
-//              the workspace (slot[co_b + i]).  Optionally computes tau first.
+// select       one workgroup per sample: every thread owns a contiguous strip
+//              of candidates, counts the strip's survivors, a wave scan plus a
+//              4-entry LDS scan gives each strip its output position, and the
+//              strip writes its survivors' candidate-local indices, ascending,
+//              to the sample's slot of the workspace (slot[co_b + i]).
+//              Optionally computes tau first.
 // pack_gather  grid (G, sample): every workgroup forms its sample's packed
 //              offset (exclusive sum of the counts before it), writes the
 //              packed survivor list (through index_map when given) and
@@ -42,7 +43,10 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     float lambda, int reduce, float* __restrict__ tau_out, int* __restrict__ slot,
     int* __restrict__ count)
 {
-    __shared__ int wcount[kSelThreads / kWave];
+    // Thread t owns the contiguous strip [t*P, t*P + P) of the sample's candidates:
+    // it counts its survivors, one block-wide exclusive scan gives every strip its
+    // output position, and the strip writes its survivors in ascending order.
+    __shared__ int wsum[kSelThreads / kWave];
     __shared__ float tau_s;
     const int b = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -62,27 +66,29 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     __syncthreads();
     const float tau = tau_s;
     const float* sv = scores + kb + p.R;
-    int base = 0;
-    for (int v0 = 0; v0 < N; v0 += kSelThreads) {
-        const int v = v0 + tid;
-        const bool keep = v < N && sv[v] >= tau;
-        const unsigned long long mask = __ballot(keep);
-        const int pos = __builtin_amdgcn_mbcnt_hi((unsigned)(mask >> 32),
-                                                  __builtin_amdgcn_mbcnt_lo((unsigned)mask, 0u));
-        if (lane == 0) wcount[wave] = __popcll(mask);
-        __syncthreads();
-        int pre = 0, tot = 0;
+    const int P = (N + kSelThreads - 1) / kSelThreads;
+    const int v0 = min(N, tid * P), v1 = min(N, v0 + P);
+    int cnt = 0;
+    for (int v = v0; v < v1; ++v) cnt += sv[v] >= tau ? 1 : 0;
+    // Inclusive scan inside the wave, then across the waves.
+    int inc = cnt;
 #pragma unroll
-        for (int w = 0; w < kSelThreads / kWave; ++w) {
-            const int cw = wcount[w];
-            pre += w < wave ? cw : 0;
-            tot += cw;
-        }
-        if (keep) slot[co + base + pre + pos] = v;
-        base += tot;
-        __syncthreads();
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int o = __shfl_up(inc, off);
+        if (lane >= off) inc += o;
     }
-    if (tid == 0) count[b] = base;
+    if (lane == kWave - 1) wsum[wave] = inc;
+    __syncthreads();
+    int base = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < kSelThreads / kWave; ++w) {
+        base += w < wave ? wsum[w] : 0;
+        total += wsum[w];
+    }
+    int pos = base + inc - cnt;
+    for (int v = v0; v < v1; ++v)
+        if (sv[v] >= tau) slot[co + pos++] = v;
+    if (tid == 0) count[b] = total;
 }
 
 __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
@@ -134,8 +140,21 @@ __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
         char* dst = rt.dst + (long long)(off + i) * rt.dst_stride;
         const long long nb = rt.row_bytes;
         if (rows.vec16) {
-            for (long long o = (long long)lane * 16; o < nb; o += 16 * kWave)
-                *reinterpret_cast<uint4*>(dst + o) = *reinterpret_cast<const uint4*>(src + o);
+            // Four 16-byte loads in flight per lane before the stores.
+            constexpr long long step = 16 * kWave;
+            long long o = (long long)lane * 16;
+            for (; o + 3 * step < nb; o += 4 * step) {
+                const u32x4 a0 = *reinterpret_cast<const u32x4*>(src + o);
+                const u32x4 a1 = *reinterpret_cast<const u32x4*>(src + o + step);
+                const u32x4 a2 = *reinterpret_cast<const u32x4*>(src + o + 2 * step);
+                const u32x4 a3 = *reinterpret_cast<const u32x4*>(src + o + 3 * step);
+                *reinterpret_cast<u32x4*>(dst + o) = a0;
+                *reinterpret_cast<u32x4*>(dst + o + step) = a1;
+                *reinterpret_cast<u32x4*>(dst + o + 2 * step) = a2;
+                *reinterpret_cast<u32x4*>(dst + o + 3 * step) = a3;
+            }
+            for (; o < nb; o += step)
+                *reinterpret_cast<u32x4*>(dst + o) = *reinterpret_cast<const u32x4*>(src + o);
         } else {
             for (long long o = (long long)lane * 4; o < nb; o += 4 * kWave)
                 *reinterpret_cast<uint32_t*>(dst + o) = *reinterpret_cast<const uint32_t*>(src + o);
