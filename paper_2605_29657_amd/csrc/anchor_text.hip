@@ -74,6 +74,21 @@ __device__ __forceinline__ u32x4 frag16(const uint16_t* row, int kk, int hi) {
 __device__ __forceinline__ void dma16(const void* gsrc, void* lds_base) {
     __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
 }
+// The same copy with a wave-uniform base address and a 32-bit per-lane byte offset,
+// issued as inline assembly: the compiler does not see it, so it neither counts it
+// among the wave's outstanding loads nor makes later LDS reads wait for it.  The
+// caller orders it explicitly (wait_vmem + barrier before the copied data is read).
+// lds is the wave-uniform LDS byte address of lane 0's 16 bytes.
+__device__ __forceinline__ void dma16_async(const void* base, uint32_t voff, uint32_t lds) {
+    asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
+                 :: "v"(voff), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
+}
+// Mark registers as produced here: loads into them must have landed before this
+// point, and the compiler keeps no outstanding-load bookkeeping for them beyond it.
+__device__ __forceinline__ void settle(u32x4& v) { asm volatile("" : "+v"(v)); }
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+    return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
+}
 // Wait until every global load of this wave (including LDS copies) has landed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
@@ -263,9 +278,13 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     u32x4* qt = reinterpret_cast<u32x4*>(smem_raw);                         // [2][NCH][128]
     float* l2t = reinterpret_cast<float*>(smem_raw + 2 * QTILE * 16);       // [H][128]
 
-    // Samples in reverse order: the statistics pass streamed sample B-1 last, so its
-    // keys are the likeliest to still sit in the memory-side cache.
-    const int c = blockIdx.x, b = p.B - 1 - (int)blockIdx.y;
+    // Task = (sample, key chunk), XCD-aware: the chunks of one sample run on one XCD
+    // and share its L2 for the query tiles.  Samples in reverse order: the statistics
+    // pass streamed sample B-1 last, so its keys are the likeliest to still sit in the
+    // memory-side cache.
+    const int nchunk = (p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg;
+    const int task = xcd_remap((int)blockIdx.x, nchunk * p.B);
+    const int c = task % nchunk, b = p.B - 1 - task / nchunk;
     const int S = keys_of(p, b);
     const int s_lo = c * kTxtKeysPerWg;
     if (s_lo >= S) return;
@@ -284,23 +303,40 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     // Rows past T_b are clamped (their lse2 is +inf, so they weigh exactly 0); the pad
     // chunk past d (HALF) reads chunk 0 instead, harmless because the matching key
     // chunk is zero.
-    auto copy_q = [&](int hh, int t0, int buf) {
-        hh = min(hh, H - 1);
+    // Per-lane byte offsets of the two 64-row halves of the row block (set_rows); a
+    // copy adds its chunk's byte offset (wave-uniform) and a head moves the base.
+    uint32_t roff[2];
+    auto set_rows = [&](int t0) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) roff[r] = (uint32_t)(min(t0 + 64 * r + lane, T - 1) * H * d) * 2u;
+    };
+    const char* qsample = reinterpret_cast<const char*>(q + (size_t)qb * H * d);
+    const uint32_t qt_lds = lds_addr(qt);
+    auto copy_q = [&](int hh, int buf) {
+        const char* base = qsample + (size_t)min(hh, H - 1) * d * 2;
 #pragma unroll
         for (int j = 0; j < COPIES; ++j) {
             const int u = wave * COPIES + j;
             const int ch = u >> 1, r0 = (u & 1) * 64;
-            const int t = min(t0 + r0 + lane, T - 1);
             const int e = (HALF && ch == NCH - 1) ? 0 : ch * 8;
-            dma16(q + ((size_t)(qb + t) * H + hh) * d + e, qt + (buf * NCH + ch) * kTxtRows + r0);
+            dma16_async(base, roff[u & 1] + (uint32_t)(e * 2),
+                        qt_lds + (uint32_t)(((buf * NCH + ch) * kTxtRows + r0) * 16));
         }
     };
+    // Key fragments: lane offset within the sample's key rows, fixed; the head picks the base.
     const int kclamp = min(wkey0 + lo, S - 1);        // keys past S_b are never written
+    const uint32_t koff = (uint32_t)(kclamp * Hkv * d) * 2u;
+    const char* ksample = reinterpret_cast<const char*>(k + (size_t)kb0 * Hkv * d);
     auto load_k = [&](int hh, u32x4 (&kf)[DS]) {
-        const int gg = min(hh, H - 1) / group;
-        const uint16_t* krow = k + ((size_t)(kb0 + kclamp) * Hkv + gg) * d;
+        const char* base = ksample + (size_t)(min(hh, H - 1) / group) * d * 2;
 #pragma unroll
-        for (int kk = 0; kk < DS; ++kk) kf[kk] = frag16<DS, HALF>(krow, kk, hi);
+        for (int kk = 0; kk < DS; ++kk) {
+            const bool pad = HALF && kk == DS - 1 && hi;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(
+                base + koff + (uint32_t)((kk * 16 + (pad ? 0 : hi * 8)) * 2));
+            const u32x4 zero = {0u, 0u, 0u, 0u};
+            kf[kk] = pad ? zero : v;
+        }
     };
 
     float vmax[MULTI ? 16 : 1], rsum[MULTI ? 16 : 1];
@@ -323,9 +359,12 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
             l2t[i] = v;
         }
         u32x4 k0[DS], k1[DS];
-        copy_q(0, t0, 0);
+        set_rows(t0);
         load_k(0, k0);
+        copy_q(0, 0);
         wait_vmem();
+#pragma unroll
+        for (int kk = 0; kk < DS; ++kk) settle(k0[kk]);
         __syncthreads();
 
 #pragma unroll
@@ -339,7 +378,11 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
         // copies and synchronise.
         auto head = [&](int h, const u32x4 (&kf)[DS], u32x4 (&kn)[DS]) {
             const int buf = h & 1;
-            copy_q(h + 1, t0, buf ^ 1);
+            // Nothing of this wave is in flight here except compiler reloads; waiting for
+            // them now keeps the compiler from waiting inside the head, where that wait
+            // would also cover the copies issued next.
+            wait_vmem();
+            copy_q(h + 1, buf ^ 1);
             load_k(h + 1, kn);
             if (wactive) {
                 const u32x4* qb_ = qt + buf * NCH * kTxtRows;
@@ -435,7 +478,7 @@ static hipError_t score_launch(const Prob& p, const void* q, const void* k, cons
         reinterpret_cast<const void*>(&text_score_kernel<DS, HALF, MULTI>),
         hipFuncAttributeMaxDynamicSharedMemorySize, (int)kScoreSmemMax);
     if (attr != hipSuccess) return attr;
-    dim3 grid((p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg, p.B);
+    dim3 grid((p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg * p.B);
     hipLaunchKernelGGL((text_score_kernel<DS, HALF, MULTI>), grid, dim3(kScoreThreads), smem, s, p,
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
                        lse_natural, scores);

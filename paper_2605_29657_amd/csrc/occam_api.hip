@@ -59,6 +59,10 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
     size_t off = 0;
     if (P.text) {
         if (!bf16 || d > 128) return OCCAM_ERR_UNSUPPORTED;
+        // The scoring kernel addresses a sample's rows and keys with 32-bit byte offsets.
+        if ((long long)max_rows * H * d * 2 >= (1LL << 32) ||
+            (R + (long long)max_cands) * x.num_kv_heads * d * 2 >= (1LL << 32))
+            return OCCAM_ERR_UNSUPPORTED;
         if (text_score_smem(H, ((d + 15) / 16) * 16) > kScoreSmemMax) return OCCAM_ERR_UNSUPPORTED;
         P.off_lse2 = off; off = align_up(off + (size_t)rows_cap * H * sizeof(float));
     } else {

@@ -80,6 +80,18 @@ constexpr int kTxtKeysPerWg = 128;   // score kernel: 4 key blocks of 32
 constexpr int kSelThreads = 256;
 constexpr int kGatherThreads = 256;
 
+// The chip dispatches consecutive workgroups of a launch round-robin over its 8
+// XCDs, each with its own L2.  xcd_remap turns a linear workgroup id into a task
+// index such that each XCD receives one contiguous range of tasks (XCD x gets
+// ranges of q+1 tasks for x < r, q otherwise, with total = 8 q + r), so tasks that
+// share data (the key chunks of one sample share its query tiles) meet in one L2.
+constexpr int kXcds = 8;
+__device__ __forceinline__ int xcd_remap(int id, int total) {
+    const int q = total / kXcds, r = total % kXcds;
+    const int x = id % kXcds, j = id / kXcds;
+    return x < r ? x * (q + 1) + j : r * (q + 1) + (x - r) * q + j;
+}
+
 // Dynamic LDS of the text-row scoring kernel: two query tiles (128 rows x d bf16)
 // and the [H][128] float normaliser tile; at most kScoreSmemMax.
 constexpr size_t kScoreSmemMax = 160 * 1024;
