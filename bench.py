@@ -77,6 +77,17 @@ def cpu_baseline(name, lam1, lam2, budget_s=15.0, max_samples=256):
                       "%.1f s" % (done, name, t_total)}
 
 
+def score_source_sha256() -> str:
+    """sha256 of the sources the Stage II scoring kernel is built from."""
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2605_29657_amd", "csrc")
+    h = hashlib.sha256()
+    for f in ("anchor_text.hip", "occam_internal.hpp"):
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
 def reference_lse(torch, txt, dt):
     """Per-(row, head) natural log-sum-exp of a uniform text stage, float32 on the device.
 
@@ -217,7 +228,10 @@ def main():
     if os.path.exists(tpath):
         with open(tpath) as f:
             tj = json.load(f)
-        if tj.get("kernel") == "text_score" and tj.get("workload") == name:
+        # The counters describe the kernel source they were taken on: report them only
+        # while that source is unchanged.
+        if (tj.get("kernel") == "text_score" and tj.get("workload") == name and
+                tj.get("source_sha256") == score_source_sha256()):
             traffic = tj.get("bytes_per_launch")
 
     rec = {
