@@ -138,6 +138,134 @@ __global__ __launch_bounds__(kClsThreads) void cls_logits_kernel(
     }
 }
 
+// Sum over aligned groups of N lanes (N = 1, 2, 4, 8, 16), every lane of a group
+// receiving the group's sum; DPP moves inside 16-lane rows, fixed order.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+template <int N>
+__device__ __forceinline__ float lane_group_sum(float x) {
+    if constexpr (N >= 2) x += dpp_f32<0xB1>(x);     // quad_perm [1,0,3,2]
+    if constexpr (N >= 4) x += dpp_f32<0x4E>(x);     // quad_perm [2,3,0,1]
+    if constexpr (N >= 8) x += dpp_f32<0x141>(x);    // row_half_mirror
+    if constexpr (N >= 16) x += dpp_f32<0x140>(x);   // row_mirror
+    return x;
+}
+
+// Streaming form of cls_logits for H == Hkv with NC (a power of two <= 16) 16-byte
+// chunks per head and NJ = H * NC / 64 wave loads per key row.  Lane l owns chunks
+// ci = l + 64 j of every key row (head ci / NC, part ci % NC) and keeps the matching
+// query elements in registers.  Each wave walks its keys KB at a time (KB rows of
+// coalesced 1 KB loads in flight), reduces the per-chunk partial dot products over
+// the NC lanes of a head with DPP, writes the scaled logit and folds it into a
+// per-head online (max, sum exp) pair held by those lanes.  The four waves' pairs are
+// merged in a fixed order at the end.
+template <bool BF16, int NC, int NJ>
+__global__ __launch_bounds__(kClsThreads) void cls_stream_kernel(
+    Prob p, const void* __restrict__ qv, const void* __restrict__ kv,
+    float* __restrict__ logits, float2* __restrict__ stats, int kpw, int nchunks)
+{
+    constexpr int CE = BF16 ? 8 : 4;                 // elements per 16-byte chunk
+    constexpr int KB = 4;                            // key rows in flight per wave
+    constexpr int NW = kClsThreads / kWave;
+    __shared__ float red_m[NW][64], red_z[NW][64];
+    const int c = blockIdx.x, b = blockIdx.y;
+    const int S = keys_of(p, b);
+    const int s0 = c * kpw;
+    if (s0 >= S) return;                             // uniform over the workgroup
+    const int nk = min(kpw, S - s0);
+    const int H = p.H, d = p.d;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float scale = p.scale;
+
+    // Query elements of this lane's chunks, as float.
+    float qf[NJ][CE];
+    const int qrow = q_begin(p, b);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int ci = lane + 64 * j;
+        const int h = ci / NC, e0 = (ci % NC) * CE;
+        if (BF16) {
+            const uint16_t* q16 = static_cast<const uint16_t*>(qv) + ((size_t)qrow * H + h) * d + e0;
+#pragma unroll
+            for (int e = 0; e < CE; ++e) qf[j][e] = __uint_as_float(static_cast<uint32_t>(q16[e]) << 16);
+        } else {
+            const float* q32 = static_cast<const float*>(qv) + ((size_t)qrow * H + h) * d + e0;
+#pragma unroll
+            for (int e = 0; e < CE; ++e) qf[j][e] = q32[e];
+        }
+    }
+
+    float m[NJ], z[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) { m[j] = -INFINITY; z[j] = 0.f; }
+    const u32x4* kbase = static_cast<const u32x4*>(kv) + ((size_t)k_begin(p, b) + s0) * (NJ * 64);
+    float* lout = logits + ((size_t)k_begin(p, b) + s0) * H;
+
+    for (int k0 = wave * KB; k0 < nk; k0 += NW * KB) {
+        u32x4 w[KB][NJ];
+#pragma unroll
+        for (int i = 0; i < KB; ++i) {
+            const int key = min(k0 + i, nk - 1);     // clamped rows are loaded, not used
+#pragma unroll
+            for (int j = 0; j < NJ; ++j)
+                w[i][j] = __builtin_nontemporal_load(kbase + (size_t)key * (NJ * 64) + lane + 64 * j);
+        }
+#pragma unroll
+        for (int i = 0; i < KB; ++i) {
+            const bool valid = k0 + i < nk;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                float kf[CE];
+                if (BF16) {
+                    kf[0] = bf16_lo(w[i][j].x); kf[1] = bf16_hi(w[i][j].x);
+                    kf[2] = bf16_lo(w[i][j].y); kf[3] = bf16_hi(w[i][j].y);
+                    kf[4] = bf16_lo(w[i][j].z); kf[5] = bf16_hi(w[i][j].z);
+                    kf[6] = bf16_lo(w[i][j].w); kf[7] = bf16_hi(w[i][j].w);
+                } else {
+                    kf[0] = __uint_as_float(w[i][j].x); kf[1] = __uint_as_float(w[i][j].y);
+                    kf[2] = __uint_as_float(w[i][j].z); kf[3] = __uint_as_float(w[i][j].w);
+                }
+                float acc = 0.f;
+#pragma unroll
+                for (int e = 0; e < CE; ++e) acc = fmaf(qf[j][e], kf[e], acc);
+                const float l = lane_group_sum<NC>(acc) * scale;
+                if (valid) {
+                    const int ci = lane + 64 * j;
+                    if (ci % NC == 0) lout[(size_t)(k0 + i) * H + ci / NC] = l;
+                    if (l > m[j]) {
+                        z[j] = z[j] * cls_exp<BF16>(m[j] - l) + 1.f;
+                        m[j] = l;
+                    } else {
+                        z[j] += cls_exp<BF16>(l - m[j]);
+                    }
+                }
+            }
+        }
+    }
+
+    // Fixed-order merge of the waves' pairs (a wave with no keys holds (-inf, 0)).
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int ci = lane + 64 * j;
+        if (ci % NC == 0) { red_m[wave][ci / NC] = m[j]; red_z[wave][ci / NC] = z[j]; }
+    }
+    __syncthreads();
+    for (int h = threadIdx.x; h < H; h += kClsThreads) {
+        float mm = red_m[0][h], zz = red_z[0][h];
+        for (int w2 = 1; w2 < NW; ++w2) {
+            const float mo = red_m[w2][h], zo = red_z[w2][h];
+            const float mn = fmaxf(mm, mo);
+            if (mn != -INFINITY) {
+                zz = zz * cls_exp<BF16>(mm - mn) + zo * cls_exp<BF16>(mo - mn);
+                mm = mn;
+            }
+        }
+        stats[((size_t)b * nchunks + c) * H + h] = make_float2(mm, zz);
+    }
+}
+
 template <bool BF16>
 __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
     Prob p, const float* __restrict__ logits, const float2* __restrict__ stats,
@@ -206,9 +334,42 @@ static size_t cls_logits_smem(const Prob& p, int bf16, int kpw) {
                             (size_t)kpw * p.H + 2 * (size_t)kClsThreads);
 }
 
+template <bool BF16, int NC>
+static hipError_t cls_stream_launch(const Prob& p, const void* q, const void* k, float* logits,
+                                    float2* stats, int kpw, hipStream_t s) {
+    const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
+    dim3 grid(nchunks, p.B);
+    switch (NC * p.Hkv / 64) {
+    case 1: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 1>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks); break;
+    case 2: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 2>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks); break;
+    case 3: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 3>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks); break;
+    case 4: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 4>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+template <bool BF16>
+static hipError_t cls_stream_nc_launch(const Prob& p, int nc, const void* q, const void* k,
+                                       float* logits, float2* stats, int kpw, hipStream_t s) {
+    switch (nc) {
+    case 1: return cls_stream_launch<BF16, 1>(p, q, k, logits, stats, kpw, s);
+    case 2: return cls_stream_launch<BF16, 2>(p, q, k, logits, stats, kpw, s);
+    case 4: return cls_stream_launch<BF16, 4>(p, q, k, logits, stats, kpw, s);
+    case 8: return cls_stream_launch<BF16, 8>(p, q, k, logits, stats, kpw, s);
+    case 16: return cls_stream_launch<BF16, 16>(p, q, k, logits, stats, kpw, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
 hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void* k,
                              float* logits, float2* stats, int kpw, hipStream_t s)
 {
+    const int nc = cls_stream_nc(p.H, p.Hkv, p.d, bf16 ? 2 : 4);
+    if (nc) {
+        return bf16 ? cls_stream_nc_launch<true>(p, nc, q, k, logits, stats, kpw, s)
+                    : cls_stream_nc_launch<false>(p, nc, q, k, logits, stats, kpw, s);
+    }
     const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
     dim3 grid(nchunks, p.B);
     const size_t smem = cls_logits_smem(p, bf16, kpw);

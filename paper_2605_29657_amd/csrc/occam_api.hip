@@ -66,12 +66,14 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
         if (text_score_smem(H, ((d + 15) / 16) * 16) > kScoreSmemMax) return OCCAM_ERR_UNSUPPORTED;
         P.off_lse2 = off; off = align_up(off + (size_t)rows_cap * H * sizeof(float));
     } else {
-        P.kpw = cls_keys_per_wg(H, d, bf16 ? 2 : 4);
+        P.kpw = cls_keys_per_wg(H, x.num_kv_heads, d, bf16 ? 2 : 4);
         const int NC = d / (bf16 ? 8 : 4);
         const size_t smem = sizeof(float) * ((size_t)H * d + (size_t)NC * x.num_kv_heads +
                                              (size_t)P.kpw * H * NC + (size_t)P.kpw * H +
                                              2 * (size_t)kClsThreads);
-        if (smem > 65536 || H > 64) return OCCAM_ERR_UNSUPPORTED;
+        if (H > 64) return OCCAM_ERR_UNSUPPORTED;
+        if (!cls_stream_nc(H, x.num_kv_heads, d, bf16 ? 2 : 4) && smem > 65536)
+            return OCCAM_ERR_UNSUPPORTED;
         const long long nchunks = (R + (long long)max_cands + P.kpw - 1) / P.kpw;
         P.off_logits = off; off = align_up(off + (size_t)keys_cap * H * sizeof(float));
         P.off_stats = off; off = align_up(off + (size_t)B * nchunks * H * sizeof(float2));

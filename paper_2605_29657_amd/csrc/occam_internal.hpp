@@ -108,7 +108,21 @@ inline size_t text_stats_smem(int d16) {
 }
 
 // Anchor-path keys per workgroup for a given row geometry.
-inline int cls_keys_per_wg(int H, int d, int elem_bytes) {
+// Streaming form of the one-row logits (cls_stream_kernel): every query head has its
+// own key head, a head is NC 16-byte chunks with NC a power of two up to 16, and a key
+// row is 1 to 4 whole 64-lane loads.  Returns NC when the form applies, else 0.
+inline int cls_stream_nc(int H, int Hkv, int d, int elem_bytes) {
+    if (H != Hkv || (d * elem_bytes) % 16 != 0) return 0;
+    const int nc = d * elem_bytes / 16;
+    if (nc != 1 && nc != 2 && nc != 4 && nc != 8 && nc != 16) return 0;
+    const int cpk = nc * Hkv;
+    if (cpk % 64 != 0 || cpk / 64 > 4) return 0;
+    return nc;
+}
+constexpr int kClsStreamKeys = 128;    // keys per workgroup of the streaming form
+
+inline int cls_keys_per_wg(int H, int Hkv, int d, int elem_bytes) {
+    if (cls_stream_nc(H, Hkv, d, elem_bytes)) return kClsStreamKeys;
     int chunks_per_head = d * elem_bytes / 16;
     int kpw = kClsPartials / (H * chunks_per_head);
     if (kpw > 64) kpw = 64;
