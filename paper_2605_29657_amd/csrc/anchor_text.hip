@@ -266,16 +266,20 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     // accumulator chains).  Two workgroups share a CU, so one workgroup's MFMAs
     // overlap the other's exponentials.
     //
-    // The query tile of a head lives in LDS chunk-major, qt[c][row] (16-byte units,
-    // c = 8-element chunk of d), double-buffered: the next head's tile is copied
-    // global -> LDS directly while the current head is computed, so the copy needs
-    // no registers and each head needs one barrier.  Reading fragment (row, c) for
-    // 32 consecutive rows touches 32 consecutive 16-byte units: no bank conflicts.
+    // The query tile of a head (128 rows x NCH 16-byte chunks) lives in LDS row-major
+    // with an XOR swizzle: chunk c of row t sits in unit t*NCH + (c ^ (t & SW)), SW =
+    // NCH - 1 when NCH is a power of two (else 0).  It is double-buffered: the next
+    // head's tile is copied global -> LDS directly (buffer loads) while the current
+    // head is computed, so the copy needs no registers and each head needs one
+    // barrier.  A copy writes 64 consecutive units, i.e. reads whole 256-byte row
+    // slices from memory; an MFMA fragment read (32 rows, one chunk each) touches 16
+    // distinct 16-byte bank groups per 16 lanes.
     constexpr int NCH = 2 * DS;                                   // 16-byte chunks per row
     constexpr int QTILE = kTxtRows * NCH;                         // 16-byte units per tile
     constexpr int COPIES = QTILE / kWave / (kScoreThreads / kWave);  // per wave per tile
+    constexpr int SW = (NCH & (NCH - 1)) == 0 ? NCH - 1 : 0;
     extern __shared__ __attribute__((aligned(16))) char smem_raw[];
-    u32x4* qt = reinterpret_cast<u32x4*>(smem_raw);                         // [2][NCH][128]
+    u32x4* qt = reinterpret_cast<u32x4*>(smem_raw);                         // [2][QTILE]
     float* l2t = reinterpret_cast<float*>(smem_raw + 2 * QTILE * 16);       // [H][128]
 
     // Task = (sample, key chunk), XCD-aware: the chunks of one sample run on one XCD
@@ -299,30 +303,34 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     const int R = p.R;
 
     // Copy head hh's query tile (rows t0..t0+127) into buffer buf.  Copy j of this
-    // wave covers chunk c = u / 2 and rows 64 (u % 2) .. +64 with u = wave*COPIES + j.
-    // Rows past T_b are clamped (their lse2 is +inf, so they weigh exactly 0); the pad
-    // chunk past d (HALF) reads chunk 0 instead, harmless because the matching key
-    // chunk is zero.
-    // Per-lane byte offsets of the two 64-row halves of the row block (set_rows); a
-    // copy adds its chunk's byte offset (wave-uniform) and a head moves the base.
-    uint32_t roff[2];
+    // wave fills units U = (wave*COPIES + j)*64 + lane: row t = U / NCH, the chunk
+    // stored there is (U % NCH) ^ (t & SW).  Rows past T_b are clamped (their lse2 is
+    // +inf, so they weigh exactly 0); the pad chunk past d (HALF) reads chunk 0
+    // instead, harmless because the matching key chunk is zero.  The per-lane byte
+    // offsets are fixed for a row block (set_rows); a head only moves the base.
+    uint32_t qoff[COPIES];
+    const char* qrows = nullptr;
     auto set_rows = [&](int t0) {
 #pragma unroll
-        for (int r = 0; r < 2; ++r) roff[r] = (uint32_t)(min(t0 + 64 * r + lane, T - 1) * H * d) * 2u;
+        for (int j = 0; j < COPIES; ++j) {
+            const int U = (wave * COPIES + j) * kWave + lane;
+            const int t = min(U / NCH, T - t0 - 1), ch = (U % NCH) ^ ((U / NCH) & SW);
+            const int e = (HALF && ch == NCH - 1) ? 0 : ch * 8;
+            qoff[j] = (uint32_t)(t * H * d + e) * 2u;
+        }
+        qrows = reinterpret_cast<const char*>(q + ((size_t)qb + t0) * H * d);
     };
-    const char* qsample = reinterpret_cast<const char*>(q + (size_t)qb * H * d);
     const uint32_t qt_lds = lds_addr(qt);
     auto copy_q = [&](int hh, int buf) {
-        const char* base = qsample + (size_t)min(hh, H - 1) * d * 2;
+        const char* base = qrows + (size_t)min(hh, H - 1) * d * 2;
 #pragma unroll
-        for (int j = 0; j < COPIES; ++j) {
-            const int u = wave * COPIES + j;
-            const int ch = u >> 1, r0 = (u & 1) * 64;
-            const int e = (HALF && ch == NCH - 1) ? 0 : ch * 8;
-            dma16_async(base, roff[u & 1] + (uint32_t)(e * 2),
-                        qt_lds + (uint32_t)(((buf * NCH + ch) * kTxtRows + r0) * 16));
-        }
+        for (int j = 0; j < COPIES; ++j)
+            dma16_async(base, qoff[j],
+                        qt_lds + (uint32_t)((buf * QTILE + (wave * COPIES + j) * kWave) * 16));
     };
+    // Byte offset in a tile of fragment (row lo of a 32-row block, chunk hi) for k-step
+    // 0; k-step kk reads (qfrag ^ kk*32) with SW, (qfrag + kk*32) without.
+    const uint32_t qfrag = (uint32_t)(lo * NCH + (hi ^ (lo & SW))) * 16u;
     // Key fragments: lane offset within the sample's key rows, fixed; the head picks the base.
     const int kclamp = min(wkey0 + lo, S - 1);        // keys past S_b are never written
     const uint32_t koff = (uint32_t)(kclamp * Hkv * d) * 2u;
@@ -385,7 +393,7 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
             copy_q(h + 1, buf ^ 1);
             load_k(h + 1, kn);
             if (wactive) {
-                const u32x4* qb_ = qt + buf * NCH * kTxtRows;
+                const char* qtile = reinterpret_cast<const char*>(qt) + buf * QTILE * 16;
 #pragma unroll
                 for (int sp = 0; sp < 4; sp += 2) {
                     if (sp >= nsb) break;
@@ -393,9 +401,10 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
                     f32x16 acc0 = {}, acc1 = {};
 #pragma unroll
                     for (int kk = 0; kk < DS; ++kk) {
-                        const int ch = 2 * kk + hi;
-                        const u32x4 q0 = qb_[ch * kTxtRows + row0];
-                        const u32x4 q1 = qb_[ch * kTxtRows + row1];
+                        const uint32_t fo = SW ? (qfrag ^ (uint32_t)(kk * 32)) : qfrag + kk * 32;
+                        const char* f0 = qtile + sp * 32 * NCH * 16 + fo;
+                        const u32x4 q0 = *reinterpret_cast<const u32x4*>(f0);
+                        const u32x4 q1 = *reinterpret_cast<const u32x4*>(f0 + 32 * NCH * 16);
                         acc0 = mfma32(as_bf16x8(kf[kk]), as_bf16x8(q0), acc0);
                         acc1 = mfma32(as_bf16x8(kf[kk]), as_bf16x8(q1), acc1);
                     }
