@@ -301,6 +301,15 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     const int wkey0 = s_lo + wave * kTxtKeysPerWave;
     const bool wactive = wkey0 < S;
     const int R = p.R;
+    // Loop step hh works on head (hh + rot) mod H, rot = workgroup id mod H: a key row's
+    // head slices all sit at the same offset within 8 KB rows, so workgroups moving
+    // through the heads in step would load the same memory channels at the same time.
+    // Steps past the last head repeat the last one (clamped prefetches).
+    const int rot = (int)(blockIdx.x % (unsigned)H);
+    auto head_of = [&](int hh) {
+        const int hc = min(hh, H - 1) + rot;
+        return hc >= H ? hc - H : hc;
+    };
 
     // Copy head hh's query tile (rows t0..t0+127) into buffer buf.  Copy j of this
     // wave fills units U = (wave*COPIES + j)*64 + lane: row t = U / NCH, the chunk
@@ -322,7 +331,7 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     };
     const uint32_t qt_lds = lds_addr(qt);
     auto copy_q = [&](int hh, int buf) {
-        const char* base = qrows + (size_t)min(hh, H - 1) * d * 2;
+        const char* base = qrows + (size_t)head_of(hh) * d * 2;
 #pragma unroll
         for (int j = 0; j < COPIES; ++j)
             dma16_async(base, qoff[j],
@@ -336,7 +345,7 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     const uint32_t koff = (uint32_t)(kclamp * Hkv * d) * 2u;
     const char* ksample = reinterpret_cast<const char*>(k + (size_t)kb0 * Hkv * d);
     auto load_k = [&](int hh, u32x4 (&kf)[DS]) {
-        const char* base = ksample + (size_t)(min(hh, H - 1) / group) * d * 2;
+        const char* base = ksample + (size_t)(head_of(hh) / group) * d * 2;
 #pragma unroll
         for (int kk = 0; kk < DS; ++kk) {
             const bool pad = HALF && kk == DS - 1 && hi;
@@ -408,8 +417,8 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
                         acc0 = mfma32(as_bf16x8(kf[kk]), as_bf16x8(q0), acc0);
                         acc1 = mfma32(as_bf16x8(kf[kk]), as_bf16x8(q1), acc1);
                     }
-                    const float l20 = l2t[h * kTxtRows + row0];
-                    const float l21 = l2t[h * kTxtRows + row1];
+                    const float l20 = l2t[head_of(h) * kTxtRows + row0];
+                    const float l21 = l2t[head_of(h) * kTxtRows + row1];
 #pragma unroll
                     for (int r = 0; r < 16; ++r) {
                         abar[sp][r] += __builtin_amdgcn_exp2f(fmaf(acc0[r], c2, -l20));
