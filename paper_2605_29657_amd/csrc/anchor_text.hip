@@ -108,14 +108,16 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     // ks = w>>1 (key blocks kbi = ks (mod 4)).  The two waves of a stream consume the
     // same key blocks, so each block is copied once per pair, global -> LDS, into a
     // ring of kRing stages per stream: kRing - 1 blocks are in flight while one is
-    // used.  A block is 32 keys x NCH 16-byte chunks; LDS unit key*NCH + j holds
-    // chunk (j + key) % NCH of that key (a rotation), so the MFMA fragment reads of
-    // 32 consecutive keys spread over the banks.
+    // used.  A block is 32 keys x NCH 16-byte chunks; chunk c of key j sits in LDS
+    // unit j*NCH + (c ^ (j & SW)), SW = NCH - 1 when NCH is a power of two (else 0),
+    // so a copy writes whole 256-byte key slices and the MFMA fragment reads of 32
+    // consecutive keys spread over the banks.
     constexpr int kStreams = kStatsThreads / kWave / 2;
     constexpr int NCH = 2 * DS;                      // 16-byte chunks per key row
     constexpr int UNITS = 32 * NCH;                  // 16-byte units per block
     constexpr int COPIES = UNITS / kWave;            // = DS copies of 64 lanes per block
     constexpr int MINE0 = (COPIES + 1) / 2, MINE1 = COPIES / 2;   // copies per pair member
+    constexpr int SW = (NCH & (NCH - 1)) == 0 ? NCH - 1 : 0;
     extern __shared__ __attribute__((aligned(16))) char smem_raw[];
     u32x4* ring = reinterpret_cast<u32x4*>(smem_raw);              // [stream][stage][UNITS]
     float* red_m = reinterpret_cast<float*>(ring + kStreams * kStatsRing * UNITS);
@@ -126,7 +128,8 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     const int t0 = tblk * kTxtRows;
     if (t0 >= T) return;
     const int S = keys_of(p, b);
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int hi = lane >> 5, lo = lane & 31;
     const int rh = wave & 1, ks = wave >> 1;
     const int H = p.H, Hkv = p.Hkv, d = p.d;
@@ -151,27 +154,49 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
 
     const int nkb = (S + 31) >> 5;
     const int nmine = (nkb - ks + kStreams - 1) / kStreams;     // blocks of this stream
-    const uint16_t* kbase = k + ((size_t)kb0 * Hkv + g) * d;
-    const size_t kstride = (size_t)Hkv * d;
+    const char* kbase = reinterpret_cast<const char*>(k + ((size_t)kb0 * Hkv + g) * d);
+    const int kstride = Hkv * d;                      // elements per key row
     u32x4* sring = ring + ks * kStatsRing * UNITS;
+    const uint32_t sring_lds = lds_addr(sring);
 
     // Copy block j of this stream (clamped to the stream's last block) into its stage.
-    // Copy c of the block covers units 64c .. 64c+63; this wave issues c = rh, rh+2, ...
-    // Chunks past d (HALF) read chunk 0 of the key: their fragment is zeroed below.
+    // Copy c of the block fills units 64c .. 64c+63; this wave issues c = rh, rh+2, ...
+    // Lane offsets inside a block are fixed (key kc = u / NCH of the block, chunk
+    // (u % NCH) ^ (kc & SW)); only a block running past S_b clamps its keys.  The pad
+    // chunk past d (HALF) reads chunk 0 of the key: its fragment is zeroed below.
+    uint32_t coff[MINE0];
+#pragma unroll
+    for (int i = 0; i < MINE0; ++i) {
+        const int u = (rh + 2 * i) * kWave + lane;
+        const int kc = u / NCH, ch = (u % NCH) ^ (kc & SW);
+        const int e = (HALF && ch == NCH - 1) ? 0 : ch * 8;
+        coff[i] = (uint32_t)(kc * kstride + e) * 2u;
+    }
     auto issue = [&](int j) {
         const int jj = min(j, max(nmine - 1, 0));
-        const int kbi = ks + jj * kStreams;
-        u32x4* dst = sring + (jj % kStatsRing) * UNITS;
+        // A stream with no block of its own (nmine == 0) copies the sample's last block:
+        // every copy stays inside the sample's keys, and the stage is never read.
+        const int kbi = min(ks + jj * kStreams, nkb - 1);
+        const char* bbase = kbase + (size_t)kbi * 32 * kstride * 2;
+        const uint32_t dst = sring_lds + (uint32_t)((jj % kStatsRing) * UNITS * 16);
+        const bool full = kbi * 32 + 32 <= S;
 #pragma unroll
-        for (int c = rh; c < COPIES; c += 2) {
-            const int u = c * kWave + lane;
-            const int key = u / NCH, pos = u % NCH;
-            const int ch = (pos + key) % NCH;
-            const int kg = min(kbi * 32 + key, S - 1);
-            const int e = (HALF && ch == NCH - 1) ? 0 : ch * 8;
-            dma16(kbase + (size_t)kg * kstride + e, dst + c * kWave);
+        for (int i = 0; i < MINE0; ++i) {
+            const int c = rh + 2 * i;
+            if (c >= COPIES) break;
+            uint32_t off = coff[i];
+            if (!full) {
+                const int u = c * kWave + lane;
+                const int kc = u / NCH, ch = (u % NCH) ^ (kc & SW);
+                const int e = (HALF && ch == NCH - 1) ? 0 : ch * 8;
+                off = (uint32_t)(min(kc, S - 1 - kbi * 32) * kstride + e) * 2u;
+            }
+            dma16_async(bbase, off, dst + (uint32_t)(c * kWave * 16));
         }
     };
+    // Byte offset in a block of fragment (key lo, chunk hi) for k-step 0; k-step kk
+    // reads (kfrag ^ kk*32) with SW, (kfrag + kk*32) without.
+    const uint32_t kfrag = (uint32_t)(lo * NCH + (hi ^ (lo & SW))) * 16u;
 
     // One key block: MFMA logits from the LDS stage, then the online (max, sum) update.
     auto block = [&](int kbi, const u32x4* blk) {
@@ -179,8 +204,8 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
         u32x4 kf[DS];
 #pragma unroll
         for (int kk = 0; kk < DS; ++kk) {
-            const int ch = 2 * kk + hi;
-            const u32x4 v = blk[lo * NCH + (ch - lo % NCH + NCH) % NCH];
+            const uint32_t fo = SW ? (kfrag ^ (uint32_t)(kk * 32)) : kfrag + kk * 32;
+            const u32x4 v = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(blk) + fo);
             const u32x4 zero = {0u, 0u, 0u, 0u};
             kf[kk] = (HALF && kk == DS - 1 && hi) ? zero : v;
         }
