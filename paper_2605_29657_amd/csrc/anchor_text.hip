@@ -15,16 +15,22 @@
 //             4th block of 32 keys, keeps the 128 query rows of the head as
 //             MFMA B fragments in registers, and maintains an online
 //             (max, sum 2^x) pair per row; pairs are merged across the two
-//             lane halves and the 4 waves in a fixed order.  Writes the base-2
-//             log-sum-exp lse2[row, head] of x = logit * log2(e).
-// text_score  grid (block of 128 keys, sample).  Each wave owns 32 keys.  For
-//             every head the 128 x d query tile is staged in LDS (the next
-//             head's tile is prefetched into registers during the current
-//             head's MFMAs) and p = 2^(x - lse2) is accumulated over heads per
-//             (key, row).  Afterwards the row reduction of Eq. text_scoring is
-//             applied: max over rows for visual keys, mean for registers,
-//             both over the head mean (1/H).  Rows beyond T_b carry
-//             lse2 = +inf and so contribute exactly 0.
+//             lane halves and the 4 key streams in a fixed order.  Key blocks
+//             reach LDS through direct global -> LDS copies (a 4-stage ring
+//             per stream).  Writes the base-2 log-sum-exp lse2[row, head] of
+//             x = logit * log2(e).
+// text_score  one workgroup per (sample, block of 128 keys).  Each wave owns 32
+//             keys.  For every head the 128 x d query tile is copied global ->
+//             LDS (double-buffered) and the wave's key fragments are loaded into
+//             registers one head ahead, while p = 2^(x - lse2) of the current
+//             head is accumulated over heads per (key, row).  Afterwards the row
+//             reduction of Eq. text_scoring is applied: max over rows for visual
+//             keys, mean for registers, both over the head mean (1/H).  Rows
+//             beyond T_b carry lse2 = +inf and so contribute exactly 0.
+//
+// The LDS copies are issued as inline global_load_lds so that the compiler does
+// not fold them into its own memory-counter waits; each kernel waits for them
+// explicitly (s_waitcnt vmcnt, then a barrier) before the stage is read.
 //
 // When the caller supplies its own natural-log normaliser (row_lse), text_stats
 // is skipped and text_score reads lse2 = row_lse * log2(e).
@@ -69,11 +75,6 @@ __device__ __forceinline__ u32x4 frag16(const uint16_t* row, int kk, int hi) {
     return pad ? zero : v;
 }
 
-// Copy 16 bytes per lane straight from global memory into LDS (gfx950
-// global_load_lds_dwordx4): lane l of the wave writes lds_base + 16 l.
-__device__ __forceinline__ void dma16(const void* gsrc, void* lds_base) {
-    __builtin_amdgcn_global_load_lds(gsrc, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
-}
 // The same copy with a wave-uniform base address and a 32-bit per-lane byte offset,
 // issued as inline assembly: the compiler does not see it, so it neither counts it
 // among the wave's outstanding loads nor makes later LDS reads wait for it.  The
@@ -83,12 +84,12 @@ __device__ __forceinline__ void dma16_async(const void* base, uint32_t voff, uin
     asm volatile("s_mov_b32 m0, %2\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, %1"
                  :: "v"(voff), "s"(base), "s"(__builtin_amdgcn_readfirstlane(lds)) : "memory");
 }
-// Mark registers as produced here: loads into them must have landed before this
-// point, and the compiler keeps no outstanding-load bookkeeping for them beyond it.
-__device__ __forceinline__ void settle(u32x4& v) { asm volatile("" : "+v"(v)); }
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
     return __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)p);
 }
+// Make the compiler treat v as produced here: a load into v must be complete before
+// this point (the compiler inserts the wait), and no later code waits for it again.
+__device__ __forceinline__ void settle(u32x4& v) { asm volatile("" : "+v"(v)); }
 // Wait until every global load of this wave (including LDS copies) has landed.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
