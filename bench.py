@@ -29,6 +29,9 @@ import numpy as np  # noqa: E402
 
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, datasheet
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16, datasheet
+# v_exp_f32 issue rate: 8 lanes per clock per SIMD x 1024 SIMDs x 2.4 GHz (a probe on the
+# MI355X measured 18.8 T/s).
+EXP_PEAK_TPS = 8 * 1024 * 2.4e9 / 1e12
 
 
 def log(*a):
@@ -77,6 +80,62 @@ def cpu_baseline(name, lam1, lam2, budget_s=15.0, max_samples=256):
                       "%.1f s" % (done, name, t_total)}
 
 
+def mutual_stage1(torch, steps: int, warmup: int, with_cpu: bool) -> dict:
+    """The mutual-scoring Stage I (Eq. mutual_scoring) on the Qwen3-VL-shaped batch: every
+    register and visual token is an anchor row.  Fused prune with the hidden-row gather,
+    timed alone; its work is (R+N)^2 * H * d per sample, so it is graded against the bf16
+    MFMA peak (algorithmic flops count one Q K^T)."""
+    import oracle
+    from paper_2605_29657_amd import synth
+    from paper_2605_29657_amd.runner import DeviceStage
+    name = "qwen3vl_ragged"
+    with open(os.path.join(ROOT, "tests", "golden", "lambdas.json")) as f:
+        lam = float(np.float32(json.load(f)[name]["mut"]["lam"]))
+    sb = synth.make_stage(name, "mut")
+    ds = DeviceStage(sb, ragged=True)
+    for _ in range(warmup):
+        ds.prune(lam)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        ds.prune(lam)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    flops = float(np.sum(2.0 * sb.T.astype(np.float64) * (sb.N + sb.R) * sb.H * sb.d))
+    # One exponential per (anchor row, key, head) in each of the two passes over the keys.
+    exps = float(np.sum(2.0 * sb.T.astype(np.float64) * (sb.N + sb.R) * sb.H))
+    kept = ds.out["kept_count"].cpu().numpy()
+    out = {"workload": "%s mutual Stage I: B=%d, N in [%d, %d], all R+N tokens as anchor rows, "
+                       "H=%d d=%d, hidden gather" % (name, sb.B, int(sb.N.min()), int(sb.N.max()),
+                                                     sb.H, sb.d),
+           "ms": round(ms, 4), "images_s": round(sb.B / (ms * 1e-3), 1),
+           "mfma_tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+           "mfma_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+           "exp_per_s": round(exps / (ms * 1e-3) / 1e12, 2), "exp_unit": "T/s",
+           "exp_frac": round(exps / (ms * 1e-3) / 1e12 / EXP_PEAK_TPS, 4),
+           "lambda1": lam, "kept_mean": float(np.mean(kept))}
+    if with_cpu:
+        done, spent = 0, 0.0
+        while done < 16 and spent < 10.0:
+            one = synth.make_stage(name, "mut", samples=[done])
+            t0 = time.perf_counter()
+            scale = float(np.float32(1.0) / np.sqrt(np.float32(one.d)))
+            res = oracle.prune(one.q, one.k, one.q_off, one.k_off, one.H, one.Hkv, one.d, one.R,
+                               lam, dtype=one.dtype, scale=scale, row_reduce=oracle.ROWS_MEAN)
+            oracle.gather(one.payload[0].rows, res["kept_idx"], res["kept_offsets"], one.k_off,
+                          one.R)
+            spent += time.perf_counter() - t0
+            done += 1
+        out["cpu_baseline"] = {"value": round(done / spent, 3), "unit": "images/s",
+                               "cores": int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1)),
+                               "kind": "oracle",
+                               "sample": "first %d image(s) of %s, mutual scores, tau, survivors, "
+                                         "gather, %.1f s" % (done, name, spent)}
+    return out
+
+
 def score_source_sha256() -> str:
     """sha256 of the sources the Stage II scoring kernel is built from."""
     import hashlib
@@ -114,6 +173,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="llava_next")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-mutual", action="store_true",
+                    help="skip the secondary mutual-scoring Stage I measurement")
+    ap.add_argument("--mutual-only", action="store_true",
+                    help="run and print only the mutual-scoring Stage I measurement")
     ap.add_argument("--kernel-reps", type=int, default=20,
                     help="timed repetitions of the dominant kernel alone")
     ap.add_argument("--kernel-only", action="store_true",
@@ -141,6 +204,10 @@ def main():
     lam2 = float(np.float32(lams["txt"]["lam"]))
 
     t0 = time.time()
+    if args.mutual_only:
+        rec = mutual_stage1(torch, args.steps, args.warmup, not args.no_cpu_baseline)
+        print(json.dumps({"mutual_stage1": rec}), flush=True)
+        return
     if args.kernel_only:
         txt = synth.make_stage(name, "txt", payload=False)
         dt = DeviceStage(txt, ragged=txt.ragged, payload=False)
@@ -267,6 +334,13 @@ def main():
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(name, lam1, lam2)
+    if not args.no_mutual:
+        del dv, dt
+        torch.cuda.empty_cache()
+        rec["mutual_stage1"] = mutual_stage1(torch, max(5, args.steps // 5), 2,
+                                             not args.no_cpu_baseline)
+        log("mutual Stage I: %.3f ms (%.0f TFLOP/s)" % (rec["mutual_stage1"]["ms"],
+                                                       rec["mutual_stage1"]["mfma_tflops"]))
     print(json.dumps(rec), flush=True)
 
 

@@ -77,7 +77,7 @@
 extern "C" {
 #endif
 
-#define OCCAM_VERSION 1
+#define OCCAM_VERSION 2
 #define OCCAM_MAX_ROW_TENSORS 8
 
 typedef enum {
@@ -95,6 +95,14 @@ typedef enum { OCCAM_F32 = 0, OCCAM_BF16 = 1 } occam_dtype;
  * reading and equals the paper's rule at R = 1. */
 typedef enum { OCCAM_REG_MEAN = 0, OCCAM_REG_MAX = 1, OCCAM_REG_SUM = 2 } occam_reg_reduce;
 
+/* How a visual key's score is reduced over the anchor rows (registers always take
+ * the mean).  MAX: the text rows of Stage II (Sec. 3.5, Eq. text_scoring).  MEAN:
+ * the mutual-scoring Stage I for encoders without a CLS token (Sec. 3.4,
+ * Eq. mutual_scoring; Appendix Eq. stage1_mutual_appendix), where the anchor rows
+ * are the register and visual tokens themselves and every key is scored by the
+ * attention it receives on average.  With one anchor row both are the same. */
+typedef enum { OCCAM_ROWS_MAX = 0, OCCAM_ROWS_MEAN = 1 } occam_row_reduce;
+
 typedef struct {
     int32_t batch;          /* B >= 1                                                */
     int32_t num_heads;      /* H >= 1                                                */
@@ -109,6 +117,7 @@ typedef struct {
     int32_t max_cands;      /* upper bound of N_b when key_offsets != NULL           */
     int32_t dtype;          /* occam_dtype of q and k                                */
     float softmax_scale;    /* 0 => 1/sqrt(d), the scale of Eq. (1)                  */
+    int32_t visual_row_reduce; /* occam_row_reduce; 0 (MAX) when zero-initialised    */
 } occam_problem;
 
 /* One row tensor gathered with the survivors (occam_gather / occam_prune).
@@ -141,11 +150,12 @@ int32_t occam_version(void);
  * holds nothing between calls. */
 size_t occam_workspace_size(const occam_problem *problem);
 
-/* Steps 1-2 (Eq. (1); Eq. EQ:CLS; Eq. text_scoring).  For every sample, every
- * anchor row t and head h, the softmax over the R + N_b keys of
- * scale * <q[t,h], k[s, h/(H/Hkv)]> is averaged over heads; the score of a
- * visual key is the max of that average over the T_b rows, the score of a
- * register the mean over the rows (T_b = 1: the CLS row itself).
+/* Steps 1-2 (Eq. (1); Eq. EQ:CLS; Eq. text_scoring; Eq. mutual_scoring).  For
+ * every sample, every anchor row t and head h, the softmax over the R + N_b keys
+ * of scale * <q[t,h], k[s, h/(H/Hkv)]> is averaged over heads; the score of a
+ * visual key is the max (visual_row_reduce MAX) or the mean (MEAN) of that
+ * average over the T_b rows, the score of a register the mean over the rows
+ * (T_b = 1: the CLS row itself).
  * row_lse (nullable): the natural-log softmax normaliser of each (row, head)
  * over a larger key set (e.g. the LLM's full causal prefix); when given,
  * probabilities are exp(logit - row_lse) instead of the softmax over the keys

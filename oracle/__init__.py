@@ -35,6 +35,7 @@ _lib = None
 _lock = threading.Lock()
 
 REG_MEAN, REG_MAX, REG_SUM = 0, 1, 2
+ROWS_MAX, ROWS_MEAN = 0, 1      # visual keys: max over anchor rows (Stage II) or mean (mutual)
 _DTYPES = {"f32": 0, "bf16": 1}
 
 
@@ -57,7 +58,7 @@ def _load():
             lib = ctypes.CDLL(_LIB_PATH)
             p = ctypes.c_void_p
             i32, i64, f64 = ctypes.c_int, ctypes.c_int64, ctypes.c_double
-            lib.oracle_scores.argtypes = [i32, i32, i32, i32, i32, p, p, i32, p, p, f64, p, p]
+            lib.oracle_scores.argtypes = [i32, i32, i32, i32, i32, p, p, i32, p, p, f64, p, i32, p]
             lib.oracle_scores.restype = i32
             lib.oracle_threshold.argtypes = [i32, i32, p, p, f64, i32, p]
             lib.oracle_threshold.restype = i32
@@ -91,12 +92,14 @@ def bf16_to_double(bits: int) -> float:
 
 
 def scores(q, k, q_off, k_off, H: int, Hkv: int, d: int, R: int, dtype: str = "bf16",
-           scale: float | None = None, row_lse=None) -> np.ndarray:
+           scale: float | None = None, row_lse=None, row_reduce: int = ROWS_MAX) -> np.ndarray:
     """Scores of all keys: ``[sum_b (R + N_b)]`` float64, registers first per sample.
 
     One anchor row (T_b = 1) gives the CLS scores of Eq. EQ:CLS; several rows give the
     text scores of Eq. text_scoring (max over rows for visual keys, mean for registers),
-    each from the head-averaged softmax map.  ``scale`` defaults to 1/sqrt(d) (Eq. (1)).
+    or with ``row_reduce=ROWS_MEAN`` the mutual scores of Eq. mutual_scoring (mean over
+    rows for every key), each from the head-averaged softmax map.  ``scale`` defaults
+    to 1/sqrt(d) (Eq. (1)).
     """
     lib = _load()
     q_off, k_off = _offsets(q_off), _offsets(k_off)
@@ -116,7 +119,7 @@ def scores(q, k, q_off, k_off, H: int, Hkv: int, d: int, R: int, dtype: str = "b
     out = np.empty(int(k_off[-1]), dtype=np.float64)
     sc = (1.0 / np.sqrt(d)) if scale is None else float(scale)
     rc = lib.oracle_scores(B, H, Hkv, d, R, _ptr(q_off), _ptr(k_off), _DTYPES[dtype],
-                           _ptr(q), _ptr(k), sc, _ptr(lse), _ptr(out))
+                           _ptr(q), _ptr(k), sc, _ptr(lse), int(row_reduce), _ptr(out))
     if rc != 0:
         raise ValueError("oracle_scores rejected the problem (rc=%d)" % rc)
     return out
@@ -181,9 +184,10 @@ def gather(src: np.ndarray, kept_idx, kept_offsets, k_off, R: int, src_pad_rows:
 
 
 def prune(q, k, q_off, k_off, H, Hkv, d, R, lam, dtype="bf16", reduce=REG_MEAN,
-          scale=None, row_lse=None, index_map=None):
+          scale=None, row_lse=None, index_map=None, row_reduce=ROWS_MAX):
     """All steps: returns dict(scores, tau, kept_idx, kept_count, kept_offsets)."""
-    sc = scores(q, k, q_off, k_off, H, Hkv, d, R, dtype=dtype, scale=scale, row_lse=row_lse)
+    sc = scores(q, k, q_off, k_off, H, Hkv, d, R, dtype=dtype, scale=scale, row_lse=row_lse,
+                row_reduce=row_reduce)
     tau = threshold(sc, k_off, R, lam, reduce)
     kept, cnt, offs = select(sc, tau, k_off, R, index_map=index_map)
     return {"scores": sc, "tau": tau, "kept_idx": kept, "kept_count": cnt, "kept_offsets": offs}

@@ -18,7 +18,9 @@
  *                                                   averaged over heads)
  *   3. anchor-row reduction: a single CLS row is taken as is (Eq. EQ:CLS);
  *      text rows are reduced by max for visual tokens and by mean for the
- *      register                                    (Eq. text_scoring)
+ *      register                                    (Eq. text_scoring);
+ *      mutual scoring takes the mean over the rows for every key
+ *                                                  (Eq. mutual_scoring)
  *   4. threshold tau = lambda * s(r)               (Eqs. stage1_threshold_appendix,
  *                                                   stage2_set_appendix)
  *   5. keep visual tokens with s(v) >= tau; the register is never a candidate
@@ -52,6 +54,8 @@
 #define ORACLE_REG_MEAN 0
 #define ORACLE_REG_MAX 1
 #define ORACLE_REG_SUM 2
+#define ORACLE_ROWS_MAX 0
+#define ORACLE_ROWS_MEAN 1
 
 /* bfloat16 is the upper half of an IEEE binary32; widening is exact. */
 static double bf16_to_double(uint16_t bits)
@@ -83,9 +87,11 @@ double oracle_bf16_to_double(uint16_t bits) { return bf16_to_double(bits); }
 int oracle_scores(int B, int H, int Hkv, int d, int R,
                   const int64_t *q_off, const int64_t *k_off,
                   int dtype, const void *q, const void *k,
-                  double scale, const double *row_lse, double *scores)
+                  double scale, const double *row_lse, int row_reduce, double *scores)
 {
     if (B < 0 || H < 1 || Hkv < 1 || H % Hkv != 0 || d < 1 || R < 1)
+        return -1;
+    if (row_reduce != ORACLE_ROWS_MAX && row_reduce != ORACLE_ROWS_MEAN)
         return -1;
     for (int b = 0; b < B; ++b)
         if (q_off[b + 1] - q_off[b] < 1 || k_off[b + 1] - k_off[b] < R)
@@ -147,11 +153,13 @@ int oracle_scores(int B, int H, int Hkv, int d, int R,
             free(qrow);
         }
         /* Step 3: visual score = max over anchor rows of the head-mean map;
-         * register score = mean over anchor rows (Eq. text_scoring).  With one
-         * anchor row both are the CLS row itself (Eq. EQ:CLS). */
+         * register score = mean over anchor rows (Eq. text_scoring).  In the
+         * mutual-scoring form every key takes the mean over the anchor rows, the
+         * average attention it receives from all of them (Eq. mutual_scoring).
+         * With one anchor row all of these are the CLS row itself (Eq. EQ:CLS). */
         double *out = scores + k_off[b];
         for (int64_t s = 0; s < S; ++s) {
-            if (s < R) {
+            if (s < R || row_reduce == ORACLE_ROWS_MEAN) {
                 double acc = 0.0;
                 for (int64_t t = 0; t < T; ++t)
                     acc += abar[t * S + s];

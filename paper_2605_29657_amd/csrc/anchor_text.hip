@@ -470,9 +470,11 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
         }
     }
 
-    // Row reduction of Eq. text_scoring: over the lane's sub-blocks, then across the 32
-    // lanes of a lane half (fixed order).  Rows past T_b hold exact zeros.
-    const bool regs = wactive && wkey0 < R;           // only the first key block has registers
+    // Row reduction of Eq. text_scoring (visual keys: max over rows) or Eq.
+    // mutual_scoring (every key: mean over rows): over the lane's sub-blocks, then
+    // across the 32 lanes of a lane half (fixed order).  Rows past T_b hold exact zeros.
+    const bool mean_rows = p.mean_rows != 0;
+    const bool regs = wactive && (mean_rows || wkey0 < R);   // keys whose row sum is needed
     float mx[16], sm[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -495,7 +497,7 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int key = wkey0 + acc_key(r, hi);
-            if (key < S) scores[kb0 + key] = key < R ? sm[r] * invHT : mx[r] * invH;
+            if (key < S) scores[kb0 + key] = (mean_rows || key < R) ? sm[r] * invHT : mx[r] * invH;
         }
     }
 }

@@ -34,6 +34,8 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
         return OCCAM_ERR_INVALID_ARG;
     if (x.dtype != OCCAM_F32 && x.dtype != OCCAM_BF16) return OCCAM_ERR_INVALID_ARG;
     if (!(x.softmax_scale >= 0.f) || isinf(x.softmax_scale)) return OCCAM_ERR_INVALID_ARG;
+    if (x.visual_row_reduce != OCCAM_ROWS_MAX && x.visual_row_reduce != OCCAM_ROWS_MEAN)
+        return OCCAM_ERR_INVALID_ARG;
     const int max_rows = x.q_offsets ? x.max_rows : x.rows;
     const int max_cands = x.key_offsets ? x.max_cands : x.cands;
     if (max_rows < 1 || max_cands < 0) return OCCAM_ERR_INVALID_ARG;
@@ -54,6 +56,7 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
     P.p.q_off = x.q_offsets; P.p.k_off = x.key_offsets;
     P.p.max_rows = max_rows; P.p.max_cands = max_cands;
     P.p.scale = x.softmax_scale > 0.f ? x.softmax_scale : 1.0f / sqrtf((float)d);
+    P.p.mean_rows = x.visual_row_reduce == OCCAM_ROWS_MEAN;
     P.bf16 = bf16;
     P.text = max_rows > 1;
     size_t off = 0;

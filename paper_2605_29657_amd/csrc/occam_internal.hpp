@@ -21,6 +21,7 @@ struct Prob {
     const int* k_off;         // [B+1] prefix of R + N_b, or null
     int max_rows, max_cands;  // bounds of T_b and N_b
     float scale;              // softmax temperature of Eq. (1)
+    int mean_rows;            // visual keys: mean over anchor rows (1) or max (0)
 };
 
 __device__ __forceinline__ int q_begin(const Prob& p, int b) {

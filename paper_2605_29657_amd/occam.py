@@ -22,6 +22,7 @@ LIB_PATH = os.path.join(_HERE, "liboccam.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 F32, BF16 = 0, 1
 REG_MEAN, REG_MAX, REG_SUM = 0, 1, 2
+ROWS_MAX, ROWS_MEAN = 0, 1
 MAX_ROW_TENSORS = 8
 
 EXPORTS = ("occam_status_string", "occam_version", "occam_workspace_size", "occam_score",
@@ -41,7 +42,7 @@ class _Problem(ctypes.Structure):
                 ("cands", ctypes.c_int32), ("q_offsets", ctypes.c_void_p),
                 ("key_offsets", ctypes.c_void_p), ("max_rows", ctypes.c_int32),
                 ("max_cands", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("softmax_scale", ctypes.c_float)]
+                ("softmax_scale", ctypes.c_float), ("visual_row_reduce", ctypes.c_int32)]
 
 
 class _Rows(ctypes.Structure):
@@ -115,14 +116,14 @@ class Problem:
 
     def __init__(self, batch, num_heads, num_kv_heads, head_dim, num_registers, rows=1, cands=0,
                  q_offsets=None, key_offsets=None, max_rows=0, max_cands=0, dtype=BF16,
-                 softmax_scale=0.0):
+                 softmax_scale=0.0, visual_row_reduce=ROWS_MAX):
         if isinstance(dtype, str):
             dtype = {"bf16": BF16, "f32": F32}[dtype]
         self.q_offsets, self.key_offsets = q_offsets, key_offsets   # keep alive
         self.c = _Problem(int(batch), int(num_heads), int(num_kv_heads), int(head_dim),
                           int(num_registers), int(rows), int(cands), _ptr(q_offsets),
                           _ptr(key_offsets), int(max_rows), int(max_cands), int(dtype),
-                          float(softmax_scale))
+                          float(softmax_scale), int(visual_row_reduce))
 
     @property
     def ref(self):

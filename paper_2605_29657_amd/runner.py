@@ -44,18 +44,20 @@ class DeviceStage:
         self.k = to_device(sb.k, sb.dtype, device)
         self.total_keys = int(sb.k_off[-1])
         self.total_cands = int(sb.N.sum())
+        # The mutual-scoring stage reduces every key by the mean over its anchor rows.
+        rr = occam.ROWS_MEAN if sb.stage == "mut" else occam.ROWS_MAX
         if self.ragged:
             self.q_off = _i32(sb.q_off, device)
             self.k_off = _i32(sb.k_off, device)
             self.problem = occam.Problem(sb.B, sb.H, sb.Hkv, sb.d, sb.R, q_offsets=self.q_off,
                                          key_offsets=self.k_off, max_rows=int(sb.T.max()),
                                          max_cands=int(sb.N.max()), dtype=sb.dtype,
-                                         softmax_scale=softmax_scale)
+                                         softmax_scale=softmax_scale, visual_row_reduce=rr)
         else:
             self.q_off = self.k_off = None
             self.problem = occam.Problem(sb.B, sb.H, sb.Hkv, sb.d, sb.R, rows=int(sb.T[0]),
                                          cands=int(sb.N[0]), dtype=sb.dtype,
-                                         softmax_scale=softmax_scale)
+                                         softmax_scale=softmax_scale, visual_row_reduce=rr)
         self.ws = occam.workspace(self.problem, device)
         self.out = occam.prune_outputs(sb.B, self.total_cands, self.total_keys, device)
         self.rows = []

@@ -211,9 +211,26 @@ def _workers() -> int:
     return max(1, min(16, os.cpu_count() or 1))
 
 
+def _mutual_sample(w: dict, wid: int, split: int, seed: int, b: int, shp: dict,
+                   payload: bool) -> dict:
+    """The mutual-scoring Stage I of an encoder without a CLS row: the keys and payload
+    of the vision stage, and one query row per register and visual token (their own
+    query projections, drawn independently from stream 3)."""
+    out = _stage_sample(w, wid, split, seed, b, "vis", shp, payload)
+    cfg = w["vis"]
+    rows = w["R"] + shp["N"]
+    rng = _rng(wid, split, seed, b, 3)
+    q = rng.standard_normal((rows, cfg["H"], cfg["d"]), dtype=np.float32)
+    out["q"] = _store(q, w["dtype"])
+    out["T"] = rows
+    return out
+
+
 def make_stage(name: str, stage: str, seed: int = 0, split: int = 0, B: int | None = None,
                payload: bool = True, samples=None) -> StageBatch:
-    """Inputs of one stage ("vis" or "txt") of workload ``name``.
+    """Inputs of one stage of workload ``name``: "vis" (the CLS row, Stage I), "txt"
+    (text rows, Stage II) or "mut" (every register and visual token as an anchor row,
+    the mutual-scoring Stage I; the vision stage's keys).
 
     ``B`` limits the batch to its first B samples; ``samples`` picks explicit sample
     numbers instead (each sample's bytes depend only on its own number).
@@ -221,16 +238,20 @@ def make_stage(name: str, stage: str, seed: int = 0, split: int = 0, B: int | No
     w = WORKLOADS[name]
     if stage == "txt" and w["txt"] is None:
         raise ValueError("workload %s has no text stage" % name)
+    if stage not in ("vis", "txt", "mut"):
+        raise ValueError("unknown stage %r" % stage)
     wid = w["id"]
     if samples is None:
         samples = list(range(w["B"] if B is None else B))
     samples = [int(s) for s in samples]
     shapes = [_shape(w, wid, split, seed, b) for b in samples]
+    if stage == "mut":
+        fn = lambda ib: _mutual_sample(w, wid, split, seed, ib[1], shapes[ib[0]], payload)
+    else:
+        fn = lambda ib: _stage_sample(w, wid, split, seed, ib[1], stage, shapes[ib[0]], payload)
     with ThreadPoolExecutor(_workers()) as ex:
-        parts = list(ex.map(lambda ib: _stage_sample(w, wid, split, seed, ib[1], stage,
-                                                     shapes[ib[0]], payload),
-                            list(enumerate(samples))))
-    cfg = w[stage]
+        parts = list(ex.map(fn, list(enumerate(samples))))
+    cfg = w["vis" if stage == "mut" else stage]
     R = w["R"]
     T = np.array([p["T"] for p in parts], dtype=np.int64)
     N = np.array([p["N"] for p in parts], dtype=np.int64)
@@ -242,7 +263,7 @@ def make_stage(name: str, stage: str, seed: int = 0, split: int = 0, B: int | No
                     H=cfg["H"], Hkv=cfg["Hkv"], d=cfg["d"], T=T, N=N, q_off=q_off,
                     k_off=k_off, q=q, k=k,
                     sinks=[s["sinks"] for s in shapes],
-                    planted=[s["informative"] if stage == "vis" else s["relevant"]
+                    planted=[s["relevant"] if stage == "txt" else s["informative"]
                              for s in shapes])
     if payload:
         sb.payload.append(Payload("hidden", np.concatenate([p["hidden"] for p in parts], 0), 0, 0))

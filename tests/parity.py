@@ -39,9 +39,10 @@ def f32_scale(d: int) -> float:
 
 def oracle_prune(sb: synth.StageBatch, lam: float, reduce: int = oracle.REG_MEAN, row_lse=None,
                  index_map=None) -> dict:
+    rr = oracle.ROWS_MEAN if sb.stage == "mut" else oracle.ROWS_MAX
     return oracle.prune(sb.q, sb.k, sb.q_off, sb.k_off, sb.H, sb.Hkv, sb.d, sb.R, lam,
                         dtype=sb.dtype, reduce=reduce, scale=f32_scale(sb.d), row_lse=row_lse,
-                        index_map=index_map)
+                        index_map=index_map, row_reduce=rr)
 
 
 def check_scores(g: np.ndarray, o: np.ndarray, rtol: float, what: str = "scores") -> float:
@@ -115,7 +116,7 @@ def check_rows(g: dict, sb: synth.StageBatch, which=None):
 
 
 def custom_stage(B, R, H, Hkv, d, T, N, dtype="bf16", seed=0, hidden=64, sinks=2,
-                 sink_scale=8.0) -> synth.StageBatch:
+                 sink_scale=8.0, stage=None) -> synth.StageBatch:
     """A small hand-shaped batch (edge cases) with Gaussian q/k, a few sinks and payload rows."""
     rng = np.random.default_rng(seed)
     T = np.asarray(T, dtype=np.int64)
@@ -129,7 +130,9 @@ def custom_stage(B, R, H, Hkv, d, T, N, dtype="bf16", seed=0, hidden=64, sinks=2
             idx = rng.choice(N[b], size=min(sinks, int(N[b])), replace=False)
             k[k_off[b] + R + idx] *= np.float32(sink_scale)
     store = (lambda x: synth.to_bf16_bits(x)) if dtype == "bf16" else (lambda x: x)
-    sb = synth.StageBatch(workload="custom", stage="txt" if T.max() > 1 else "vis", dtype=dtype,
+    if stage is None:
+        stage = "txt" if T.max() > 1 else "vis"
+    sb = synth.StageBatch(workload="custom", stage=stage, dtype=dtype,
                           B=B, R=R, H=H, Hkv=Hkv, d=d, T=T, N=N, q_off=q_off, k_off=k_off,
                           q=store(q), k=store(k))
     hid = store(rng.standard_normal((int(N.sum()), hidden)).astype(np.float32))

@@ -50,7 +50,7 @@ def test_library_exports_every_declared_symbol(L):
 
 
 def test_version_and_status_strings(L):
-    assert L.occam_version() == 1
+    assert L.occam_version() == 2
     for s in range(5):
         assert occam.status_string(s).startswith("OCCAM_")
     assert "unknown" in occam.status_string(77)
@@ -72,6 +72,7 @@ def ws_size(p):
     dict(head_dim=0), dict(head_dim=264), dict(num_registers=0), dict(num_registers=33),
     dict(rows=0), dict(cands=-1), dict(dtype=7), dict(softmax_scale=-1.0),
     dict(softmax_scale=float("inf")), dict(softmax_scale=float("nan")),
+    dict(visual_row_reduce=2), dict(visual_row_reduce=-1),
 ])
 def test_invalid_problems(L, kw):
     p = good_problem(**kw)
@@ -91,6 +92,13 @@ def test_unsupported_shapes(L, kw):
     assert ws_size(p) == 0
     st = L.occam_score(p.ref, FAKE, FAKE, None, FAKE, FAKE, 1 << 40, None)
     assert st == occam.ERR_UNSUPPORTED
+
+
+def test_mutual_scoring_is_a_valid_problem(L):
+    # Every token an anchor row, mean over rows (Eq. mutual_scoring).
+    p = good_problem(rows=580, cands=576, visual_row_reduce=occam.ROWS_MEAN)
+    assert ws_size(p) > 0
+    assert ws_size(p) == ws_size(good_problem(rows=580, cands=576))
 
 
 def test_workspace_size_grows_with_the_batch(L):

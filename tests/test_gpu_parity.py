@@ -102,6 +102,80 @@ def test_headline_full_batch_sampled(stage):
     check_rows(g, sb)
 
 
+# ----------------------------------------------------------------------------- mutual scoring
+# Stage I without a CLS row (Eq. mutual_scoring): every register and visual token is
+# an anchor row and each key is scored by the mean attention it receives.
+def test_mutual_llava15():
+    sb = synth.make_stage("llava15", "mut", B=3)
+    run_and_check(sb, lam_for("llava15", "mut"))
+
+
+def small_qwen_samples(n=3, limit=1500):
+    """Sample numbers of the Qwen3-VL-shaped batch whose N stays below ``limit``."""
+    out = []
+    for b in range(64):
+        sb = synth.make_stage("qwen3vl_ragged", "vis", samples=[b], payload=False)
+        if int(sb.N[0]) < limit:
+            out.append(b)
+        if len(out) == n:
+            break
+    return out
+
+
+def test_mutual_qwen3vl_ragged_d72():
+    sb = synth.make_stage("qwen3vl_ragged", "mut", samples=small_qwen_samples())
+    run_and_check(sb, lam_for("qwen3vl_ragged", "mut"))
+
+
+def test_mutual_ragged_with_an_empty_sample():
+    N = np.array([0, 37, 130])
+    sb = custom_stage(B=3, R=4, H=4, Hkv=4, d=64, T=N + 4, N=N, stage="mut", seed=11)
+    run_and_check(sb, 1.0)
+
+
+def test_mutual_at_one_row_matches_the_max_form():
+    # One anchor row: mean and max over rows are the same number.
+    sb = custom_stage(B=2, R=4, H=8, Hkv=8, d=64, T=[1, 1], N=[100, 50], seed=12)
+    a = DeviceStage(sb, ragged=True)
+    a.prune(1.2)
+    sb.stage = "mut"
+    m = DeviceStage(sb, ragged=True)
+    m.prune(1.2)
+    assert torch.equal(a.out["scores"], m.out["scores"])
+
+
+def test_mutual_headline_shape_sampled():
+    # LLaVA-NeXT-shaped encoder without a CLS row at full size: B=32 samples of 2884
+    # anchor rows x 2884 keys; two samples recomputed by the oracle.
+    name = "llava_next"
+    lam = lam_for(name, "mut")
+    sb = synth.make_stage(name, "mut")
+    ds = DeviceStage(sb, ragged=False)
+    ds.prune(lam)
+    g = ds.host()
+    pick = [3, 30]
+    sub = synth.make_stage(name, "mut", samples=pick)
+    o = oracle_prune(sub, lam)
+    rtol = RTOL[sb.dtype]
+    for j, b in enumerate(pick):
+        gs = g["scores"][sb.k_off[b]:sb.k_off[b + 1]]
+        check_scores(gs, o["scores"][sub.k_off[j]:sub.k_off[j + 1]], rtol)
+        check_scores(g["tau"][b:b + 1], o["tau"][j:j + 1], rtol, "tau")
+        gsel = dict(kept_idx=g["kept_idx"][g["kept_offsets"][b]:g["kept_offsets"][b + 1]],
+                    kept_count=g["kept_count"][b:b + 1],
+                    kept_offsets=np.array([0, g["kept_count"][b]]))
+        one = synth.make_stage(name, "mut", samples=[b], payload=False)
+        oj = dict(scores=o["scores"][sub.k_off[j]:sub.k_off[j + 1]], tau=o["tau"][j:j + 1],
+                  kept_idx=o["kept_idx"][o["kept_offsets"][j]:o["kept_offsets"][j + 1]],
+                  kept_offsets=np.array([0, o["kept_count"][j]]))
+        check_selection(gsel, oj, one, rtol)
+    # Every key's mutual score is a mean of probabilities: each sample's scores sum to 1.
+    sums = np.add.reduceat(g["scores"].astype(np.float64), sb.k_off[:-1])
+    np.testing.assert_allclose(sums, 1.0, rtol=1e-4)
+    check_bookkeeping(g, sb)
+    check_rows(g, sb)
+
+
 # ----------------------------------------------------------------------------- edge cases
 def test_ragged_with_empty_samples():
     sb = custom_stage(B=5, R=3, H=4, Hkv=4, d=64, T=[1] * 5, N=[0, 37, 0, 300, 1])

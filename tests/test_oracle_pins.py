@@ -250,6 +250,84 @@ def test_fp64_error_is_below_1e13_against_50_digit_arithmetic():
             assert abs(got[s] - float(want)) <= 1e-13 * float(want)
 
 
+# ----------------------------------------------------------------------------- mutual scoring
+def mutual_sample(T_extra=0, S=40, H=3, Hkv=3, d=16, R=2, seed=30):
+    """A self-attention sample: the anchor rows are the R + N tokens themselves (plus
+    T_extra further rows), Eq. mutual_scoring."""
+    rng = np.random.default_rng(seed)
+    T = S + T_extra
+    q = rng.standard_normal((T, H, d)).astype(np.float32)
+    k = rng.standard_normal((S, Hkv, d)).astype(np.float32)
+    return q, k
+
+
+@pytest.mark.parametrize("H,Hkv", [(1, 1), (3, 3), (4, 2)])
+def test_mutual_scores_sum_to_one(H, Hkv):
+    # Every anchor row's head-mean map sums to 1 over the keys, so the mean over rows
+    # does too; a max in place of the mean, a dropped 1/T or 1/H breaks it.
+    q, k = mutual_sample(H=H, Hkv=Hkv, seed=31 + H)
+    sc = one_sample(q, k, 2, H, Hkv, 16, row_reduce=oracle.ROWS_MEAN)
+    assert abs(sc.sum() - 1.0) < 1e-12
+
+
+def test_mutual_with_one_row_is_the_cls_score():
+    q, k = mutual_sample(seed=32)
+    a = one_sample(q[:1], k, 2, 3, 3, 16, row_reduce=oracle.ROWS_MEAN)
+    b = one_sample(q[:1], k, 2, 3, 3, 16)
+    assert np.array_equal(a, b)
+
+
+def test_mutual_uniform_attention_gives_one_over_s():
+    # q = 0: every row attends uniformly, so every key receives 1/S on average.
+    q, k = mutual_sample(seed=33)
+    sc = one_sample(np.zeros_like(q), k, 2, 3, 3, 16, row_reduce=oracle.ROWS_MEAN)
+    np.testing.assert_allclose(sc, 1.0 / k.shape[0], rtol=1e-14)
+
+
+def test_mutual_is_below_the_row_max_and_keeps_the_register_mean():
+    q, k = mutual_sample(seed=34)
+    mean = one_sample(q, k, 2, 3, 3, 16, row_reduce=oracle.ROWS_MEAN)
+    mx = one_sample(q, k, 2, 3, 3, 16)
+    assert np.all(mean <= mx + 1e-15)
+    assert np.array_equal(mean[:2], mx[:2])          # registers take the mean either way
+    assert np.any(mean[2:] < mx[2:] * 0.999)
+
+
+def test_mutual_is_invariant_to_the_order_of_the_anchor_rows():
+    q, k = mutual_sample(T_extra=5, seed=35)
+    perm = np.random.default_rng(35).permutation(q.shape[0])
+    a = one_sample(q, k, 2, 3, 3, 16, row_reduce=oracle.ROWS_MEAN)
+    b = one_sample(q[perm], k, 2, 3, 3, 16, row_reduce=oracle.ROWS_MEAN)
+    np.testing.assert_allclose(b, a, rtol=1e-13)
+
+
+def test_mutual_equals_the_column_mean_of_a_50_digit_attention_map():
+    mpmath.mp.dps = 50
+    rng = np.random.default_rng(36)
+    for trial in range(8):
+        H, d, R, N = int(rng.integers(1, 3)), 4, int(rng.integers(1, 3)), int(rng.integers(0, 7))
+        S = R + N
+        q = rng.integers(-2, 3, (S, H, d)).astype(np.float32)
+        k = rng.integers(-2, 3, (S, H, d)).astype(np.float32)
+        got = one_sample(q, k, R, H, H, d, row_reduce=oracle.ROWS_MEAN)
+        scale = mpmath.mpf(1) / mpmath.sqrt(d)
+        for s in range(S):
+            acc = mpmath.mpf(0)
+            for u in range(S):
+                for h in range(H):
+                    lg = [scale * sum(mpmath.mpf(float(q[u, h, e])) * float(k[j, h, e]) for e in range(d))
+                          for j in range(S)]
+                    acc += mpmath.exp(lg[s]) / sum(mpmath.exp(x) for x in lg) / H
+            want = acc / S
+            assert abs(got[s] - float(want)) <= 1e-13 * float(want)
+
+
+def test_oracle_rejects_an_unknown_row_reduction():
+    q, k = mutual_sample(seed=37)
+    with pytest.raises(ValueError):
+        one_sample(q, k, 2, 3, 3, 16, row_reduce=2)
+
+
 # ----------------------------------------------------------------------------- step 3
 @pytest.mark.parametrize("reduce,fn", [(oracle.REG_MEAN, np.mean), (oracle.REG_MAX, np.max),
                                        (oracle.REG_SUM, np.sum)])
