@@ -136,6 +136,34 @@ def mutual_stage1(torch, steps: int, warmup: int, with_cpu: bool) -> dict:
     return out
 
 
+def register_redirect_bench(torch, reps: int = 20) -> dict:
+    """Test-time register construction (Eq. register_redirect_appendix) at the LLaVA-NeXT
+    vision shape: 32 images x (4 registers + 2880 patches) rows of a 4096-wide bf16 MLP
+    activation, ten register channels.  Each channel element sits in its own 8 KB row,
+    so the call is bound by latency and cache-line traffic, not by its few bytes."""
+    from paper_2605_29657_amd import occam
+    B, R, N, width = 32, 4, 2880, 4096
+    h = torch.randn((B * (R + N), width), device="cuda").to(torch.bfloat16)
+    chans = torch.tensor(np.random.default_rng(0).choice(width, 10, replace=False).astype(np.int32),
+                         device="cuda")
+    p = occam.Problem(B, 16, 16, 64, R, cands=N, dtype="bf16")
+    occam.register_redirect(p, h, chans)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        occam.register_redirect(p, h, chans)
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    alg = B * 10 * (2 * N * 2 + 2)           # read + zero each visual value, write the register
+    lines = B * 10 * (R + N) * 128            # one 128-byte line per touched row and channel
+    del h
+    return {"workload": "B=%d, %d rows x %d bf16, 10 channels" % (B, R + N, width),
+            "us": round(ms * 1e3, 2), "algorithmic_bytes": alg, "line_bytes": lines,
+            "line_gbs": round(lines / (ms * 1e-3) / 1e9, 1)}
+
+
 def score_source_sha256() -> str:
     """sha256 of the sources the Stage II scoring kernel is built from."""
     import hashlib
@@ -334,6 +362,8 @@ def main():
     }
     if not args.no_cpu_baseline:
         rec["cpu_baseline"] = cpu_baseline(name, lam1, lam2)
+    rec["register_redirect"] = register_redirect_bench(torch)
+    log("register redirect: %.1f us" % rec["register_redirect"]["us"])
     if not args.no_mutual:
         del dv, dt
         torch.cuda.empty_cache()

@@ -198,6 +198,23 @@ occam_status occam_prune(const occam_problem *problem, const void *q, const void
                          int32_t *kept_offsets, void *workspace, size_t ws_bytes,
                          hipStream_t stream);
 
+/* Test-time register construction (Algorithm 1, "redirect sinks to r"; Appendix
+ * Eq. register_redirect_appendix), applied to an MLP activation tensor of the
+ * vision encoder before Stage I.  For every sample b and every listed channel k:
+ *     h[register row, k] = max over the sample's visual rows of h[v, k]
+ *     h[v, k]            = 0 for every visual row v,
+ * in place.  Rows follow the key layout of the problem: sample b owns rows
+ * ko_b .. ko_b + R + N_b - 1 (R register rows first), each `width` elements of
+ * `problem->dtype` (F32 or BF16) with `row_stride_bytes` between rows; only the
+ * register row reg_slot (in [0, R)) receives the maxima.  A sample without visual
+ * rows (N_b = 0) is left unchanged.  channels: device int32 [n_channels]
+ * (n_channels in [0, 1024]); an index outside [0, width) is ignored and a repeated
+ * index acts once.  The anchor-row fields of the problem are not used. */
+occam_status occam_register_redirect(const occam_problem *problem, void *h, int32_t width,
+                                     int64_t row_stride_bytes, const int32_t *channels,
+                                     int32_t n_channels, int32_t reg_slot,
+                                     hipStream_t stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -66,6 +66,8 @@ def _load():
             lib.oracle_select.restype = i32
             lib.oracle_gather.argtypes = [i32, i32, p, p, i64, i64, i64, p, i64, i64, p, p]
             lib.oracle_gather.restype = i32
+            lib.oracle_register_redirect.argtypes = [i32, i32, p, i32, p, i64, i64, p, i32, i32]
+            lib.oracle_register_redirect.restype = i32
             lib.oracle_neff.argtypes = [p, i64]
             lib.oracle_neff.restype = f64
             lib.oracle_bf16_to_double.argtypes = [ctypes.c_uint16]
@@ -235,3 +237,25 @@ def match_lambda(ratio_lists, k_target: float) -> float:
     if lo > 0.0 and hi > 0.0:
         return float(np.sqrt(hi * lo))
     return float(hi * 0.5 if hi > 0 else 0.0)
+
+
+def register_redirect(h, k_off, R: int, channels, reg_slot: int = 0, dtype: str = "bf16"):
+    """Test-time register construction (Algorithm 1; Eq. register_redirect_appendix) on a
+    copy of the activation tensor ``h`` ([rows, width], uint16 bf16 bits or float32).
+
+    For every listed channel k and sample b, the register row ``reg_slot`` takes the max
+    of channel k over the sample's visual rows and those rows' channel k becomes 0.
+    Returns the new tensor."""
+    lib = _load()
+    k_off = _offsets(k_off)
+    want = np.uint16 if dtype == "bf16" else np.float32
+    out = np.array(h, dtype=want, copy=True, order="C")
+    if out.ndim != 2 or out.shape[0] < k_off[-1]:
+        raise ValueError("h must be [rows >= sum_b (R + N_b), width]")
+    ch = np.ascontiguousarray(np.asarray(channels, dtype=np.int32))
+    rc = lib.oracle_register_redirect(len(k_off) - 1, R, _ptr(k_off), _DTYPES[dtype], _ptr(out),
+                                      out.shape[1], out.shape[1], _ptr(ch), int(ch.size),
+                                      int(reg_slot))
+    if rc != 0:
+        raise ValueError("oracle_register_redirect rejected the problem (rc=%d)" % rc)
+    return out

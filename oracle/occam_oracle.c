@@ -272,3 +272,65 @@ double oracle_neff(const double *alpha, int64_t n)
             h -= alpha[i] * log(alpha[i]);
     return exp(h);
 }
+
+/*
+ * Test-time register construction (Algorithm 1, "redirect sinks to r"; Appendix
+ * Eq. register_redirect_appendix), in place on an activation tensor laid out like
+ * the keys: sample b owns rows k_off[b] .. k_off[b+1]-1, R register rows first,
+ * each `width` elements, `stride` elements apart.  For every listed channel k:
+ * h[register row reg_slot, k] = max over the visual rows of h[v, k] (a zero maximum
+ * is stored as +0), then h[v, k] = 0 for every visual row.  Readings: an index
+ * outside [0, width) is ignored, a repeated index acts once (its first
+ * occurrence), a sample without visual rows is left unchanged.
+ */
+static void store_elem(void *base, int dtype, int64_t idx, double v)
+{
+    if (dtype == ORACLE_BF16) {
+        /* v is a value read from this tensor, so its bf16 encoding is exact. */
+        float f = (float)v;
+        uint32_t u;
+        memcpy(&u, &f, sizeof u);
+        ((uint16_t *)base)[idx] = (uint16_t)(u >> 16);
+    } else {
+        ((float *)base)[idx] = (float)v;
+    }
+}
+
+int oracle_register_redirect(int B, int R, const int64_t *k_off, int dtype, void *h,
+                             int64_t width, int64_t stride, const int32_t *channels,
+                             int n_channels, int reg_slot)
+{
+    if (B < 0 || R < 1 || width < 1 || stride < width || n_channels < 0 ||
+        reg_slot < 0 || reg_slot >= R)
+        return -1;
+    for (int b = 0; b < B; ++b) {
+        const int64_t first = k_off[b], N = k_off[b + 1] - k_off[b] - R;
+        if (N < 0)
+            return -1;
+        if (N == 0)
+            continue;
+        for (int j = 0; j < n_channels; ++j) {
+            const int32_t k = channels[j];
+            if (k < 0 || k >= width)
+                continue;
+            int repeat = 0;
+            for (int i = 0; i < j; ++i)
+                if (channels[i] == k)
+                    repeat = 1;
+            if (repeat)
+                continue;
+            double m = load_elem(h, dtype, (first + R) * stride + k);
+            for (int64_t v = 1; v < N; ++v) {
+                const double x = load_elem(h, dtype, (first + R + v) * stride + k);
+                if (x > m)
+                    m = x;
+            }
+            if (m == 0.0)
+                m = 0.0; /* +0 */
+            store_elem(h, dtype, (first + reg_slot) * stride + k, m);
+            for (int64_t v = 0; v < N; ++v)
+                store_elem(h, dtype, (first + R + v) * stride + k, 0.0);
+        }
+    }
+    return 0;
+}

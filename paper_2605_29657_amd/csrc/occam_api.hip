@@ -150,6 +150,26 @@ occam_status run_score(const Plan& P, const void* q, const void* k, const float*
     return hip_ok(launch_cls_scores(P.p, P.bf16, logits, stats, row_lse, scores, P.kpw, s));
 }
 
+// The key layout of a problem alone (register construction reads no anchor rows).
+occam_status key_layout(const occam_problem* pr, Prob* out, int* bf16) {
+    if (!pr) return OCCAM_ERR_INVALID_ARG;
+    const occam_problem& x = *pr;
+    if (x.batch < 1 || x.num_registers < 1 || x.num_registers > 32) return OCCAM_ERR_INVALID_ARG;
+    if (x.dtype != OCCAM_F32 && x.dtype != OCCAM_BF16) return OCCAM_ERR_INVALID_ARG;
+    const int max_cands = x.key_offsets ? x.max_cands : x.cands;
+    if (max_cands < 0) return OCCAM_ERR_INVALID_ARG;
+    if (x.key_offsets && !aligned(x.key_offsets, 4)) return OCCAM_ERR_INVALID_ARG;
+    if ((long long)x.batch * (x.num_registers + (long long)max_cands) >= (1LL << 31))
+        return OCCAM_ERR_UNSUPPORTED;
+    Prob p;
+    memset(&p, 0, sizeof p);
+    p.B = x.batch; p.R = x.num_registers; p.cands = x.cands; p.k_off = x.key_offsets;
+    p.max_cands = max_cands; p.rows = 1; p.max_rows = 1;
+    *out = p;
+    *bf16 = x.dtype == OCCAM_BF16;
+    return OCCAM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -259,6 +279,23 @@ occam_status occam_prune(const occam_problem* problem, const void* q, const void
     if (st != OCCAM_OK) return st;
     return hip_ok(launch_pack_gather(P.p, slot, kept_count, index_map, kept_idx, kept_offsets,
                                      nullptr, nullptr, rows, stream));
+}
+
+occam_status occam_register_redirect(const occam_problem* problem, void* h, int32_t width,
+                                     int64_t row_stride_bytes, const int32_t* channels,
+                                     int32_t n_channels, int32_t reg_slot, hipStream_t stream) {
+    Prob p;
+    int bf16 = 0;
+    occam_status st = key_layout(problem, &p, &bf16);
+    if (st != OCCAM_OK) return st;
+    const int64_t e = bf16 ? 2 : 4;
+    if (!h || !aligned(h, (size_t)e) || width < 1 || row_stride_bytes < width * e ||
+        row_stride_bytes % e != 0 || n_channels < 0 || n_channels > 1024 ||
+        (n_channels > 0 && (!channels || !aligned(channels, 4))) || reg_slot < 0 ||
+        reg_slot >= p.R)
+        return OCCAM_ERR_INVALID_ARG;
+    return hip_ok(launch_register_redirect(p, bf16, h, width, row_stride_bytes, channels,
+                                           n_channels, reg_slot, stream));
 }
 
 }  // extern "C"

@@ -133,6 +133,9 @@ inline int cls_keys_per_wg(int H, int Hkv, int d, int elem_bytes) {
 
 // ---------------------------------------------------------------------------
 // Launchers (defined in the .hip files).  All return hipGetLastError().
+hipError_t launch_register_redirect(const Prob& p, int bf16, void* h, int width, long long stride,
+                                    const int* channels, int n_channels, int reg_slot,
+                                    hipStream_t s);
 hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void* k,
                              float* logits, float2* stats, int kpw, hipStream_t s);
 hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const float2* stats,

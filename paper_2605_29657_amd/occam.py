@@ -26,7 +26,8 @@ ROWS_MAX, ROWS_MEAN = 0, 1
 MAX_ROW_TENSORS = 8
 
 EXPORTS = ("occam_status_string", "occam_version", "occam_workspace_size", "occam_score",
-           "occam_threshold", "occam_select", "occam_gather", "occam_prune")
+           "occam_threshold", "occam_select", "occam_gather", "occam_prune",
+           "occam_register_redirect")
 
 
 class OccamError(RuntimeError):
@@ -82,6 +83,8 @@ def lib():
         L.occam_prune.argtypes = [P, vp, vp, vp, f32, i32, vp, i32, RP, vp, vp, vp, vp, vp, vp,
                                   sz, vp]
         L.occam_prune.restype = i32
+        L.occam_register_redirect.argtypes = [P, vp, i32, ctypes.c_int64, vp, i32, i32, vp]
+        L.occam_register_redirect.restype = i32
         _lib = L
     return _lib
 
@@ -194,6 +197,17 @@ def prune(problem, q, k, lam, kept_idx, kept_count, kept_offsets, ws, reduce=REG
                              _ptr(index_map), n, arr, _ptr(scores), _ptr(tau), _ptr(kept_idx),
                              _ptr(kept_count), _ptr(kept_offsets), _ptr(ws),
                              0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def register_redirect(problem, h, channels, reg_slot=0, stream=None):
+    """occam_register_redirect on a 2-D activation tensor ``h`` ([rows, width], in place);
+    ``channels`` an int32 device tensor of channel indices."""
+    if h.dim() != 2:
+        raise ValueError("h must be a 2-D [rows, width] tensor")
+    _check(lib().occam_register_redirect(problem.ref, _ptr(h), int(h.shape[1]),
+                                         int(h.stride(0) * h.element_size()), _ptr(channels),
+                                         int(channels.numel()) if channels is not None else 0,
+                                         int(reg_slot), _stream(stream)))
 
 
 def prune_outputs(batch: int, total_cands: int, total_keys: int, device="cuda"):

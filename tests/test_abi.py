@@ -184,3 +184,21 @@ def test_binding_raises_without_the_library(monkeypatch, tmp_path):
     monkeypatch.setattr(occam, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(RuntimeError):
         occam.lib()
+
+
+def test_register_redirect_validation(L):
+    p = good_problem()
+    ok = dict(h=FAKE, width=64, stride=128, ch=FAKE, n=4, slot=0)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return L.occam_register_redirect(p.ref, a["h"], a["width"], a["stride"], a["ch"], a["n"],
+                                         a["slot"], None)
+    for bad in (dict(h=None), dict(h=FAKE + 1), dict(width=0), dict(stride=64),
+                dict(stride=129), dict(ch=None), dict(ch=FAKE + 2), dict(n=-1), dict(n=1025),
+                dict(slot=-1), dict(slot=4)):
+        assert call(**bad) == occam.ERR_INVALID_ARG, bad
+    assert L.occam_register_redirect(None, FAKE, 64, 128, FAKE, 4, 0, None) == occam.ERR_INVALID_ARG
+    # n = 0 launches nothing and succeeds, even without a channel list or a GPU.
+    assert call(ch=None, n=0) == occam.OK

@@ -588,3 +588,64 @@ def test_paper_stage1_table_lambda_zero_keeps_all_and_counts_fall():
         counts.append(int(oracle.select(sc, tau, sb.k_off, sb.R)[1][0]))
     assert counts[0] == 2880
     assert all(np.diff(counts) <= 0)
+
+
+# ----------------------------------------------------------------------------- register construction
+def redirect_case(seed=40, B=3, R=2, N=(7, 0, 12), width=9):
+    rng = np.random.default_rng(seed)
+    N = np.asarray(N)
+    k_off = np.concatenate([[0], np.cumsum(N + R)]).astype(np.int64)
+    h = rng.standard_normal((int(k_off[-1]), width)).astype(np.float32)
+    return h, k_off, R
+
+
+def test_register_redirect_moves_the_channel_max_and_zeroes_the_visual_rows():
+    h, k_off, R = redirect_case()
+    chans = [5, 1]
+    out = oracle.register_redirect(h, k_off, R, chans, reg_slot=1, dtype="f32")
+    for b in range(len(k_off) - 1):
+        lo, hi = k_off[b], k_off[b + 1]
+        vis = slice(lo + R, hi)
+        for c in range(h.shape[1]):
+            if c in chans and hi - lo > R:
+                assert out[lo + 1, c] == np.max(h[vis, c])     # numpy's max, to the bit
+                assert np.all(out[vis, c] == 0.0)
+                assert out[lo, c] == h[lo, c]                 # the other register row
+            else:
+                assert np.array_equal(out[lo:hi, c], h[lo:hi, c])
+
+
+def test_register_redirect_leaves_an_empty_sample_alone():
+    h, k_off, R = redirect_case(seed=41)
+    out = oracle.register_redirect(h, k_off, R, [0, 3], dtype="f32")
+    assert np.array_equal(out[k_off[1]:k_off[2]], h[k_off[1]:k_off[2]])
+
+
+def test_register_redirect_ignores_repeats_and_out_of_range_channels():
+    h, k_off, R = redirect_case(seed=42)
+    a = oracle.register_redirect(h, k_off, R, [2, 7, 2, -1, 9, 100], dtype="f32")
+    b = oracle.register_redirect(h, k_off, R, [2, 7], dtype="f32")
+    assert np.array_equal(a, b)
+
+
+def test_register_redirect_bf16_keeps_the_bits_and_writes_plus_zero():
+    h, k_off, R = redirect_case(seed=43)
+    h[k_off[0] + R:k_off[1], 4] = -np.abs(h[k_off[0] + R:k_off[1], 4])   # all <= 0 ...
+    h[k_off[0] + R + 3, 4] = -0.0                                       # ... max is -0
+    bits = synth.to_bf16_bits(h)
+    out = oracle.register_redirect(bits, k_off, R, [4, 6], dtype="bf16")
+    assert out[k_off[0], 4] == 0x0000                                   # +0, not 0x8000
+    vis = slice(k_off[2] + R, k_off[3])
+    want = bits[vis, 6][np.argmax(h[vis, 6])]
+    assert out[k_off[2], 6] == want
+    assert np.all(out[vis, 6] == 0)
+
+
+def test_register_redirect_absorbs_a_sink_channel():
+    # A planted high-activation channel of one patch (the sink pattern the register
+    # construction targets) ends up in the register, and no visual row keeps it.
+    h, k_off, R = redirect_case(seed=44, B=1, N=(30,), width=16)
+    h[R + 11, 9] = 80.0
+    out = oracle.register_redirect(h, k_off, R, [9], dtype="f32")
+    assert out[0, 9] == 80.0 and np.max(np.abs(out[R:, 9])) == 0.0
+    assert np.linalg.norm(out[R + 11]) < 0.5 * np.linalg.norm(h[R + 11])
