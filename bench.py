@@ -164,6 +164,36 @@ def register_redirect_bench(torch, reps: int = 20) -> dict:
             "line_gbs": round(lines / (ms * 1e-3) / 1e9, 1)}
 
 
+def budget_matching_bench(torch, reps: int = 20) -> dict:
+    """Budget matching (Eq. lambda2_budget_matching_appendix) over a calibration set of 64
+    LLaVA-NeXT samples (4 registers + 2880 candidates each, 184,320 ratios) at a target of
+    576 kept per sample.  Scores are log-normal with a register score near the top, the
+    shape the text scores take.  One workgroup runs the whole selection, so the call is
+    bound by that workgroup's passes over the ratios, not by HBM."""
+    from paper_2605_29657_amd import occam
+    B, R, N = 64, 4, 2880
+    g = torch.Generator(device="cuda").manual_seed(0)
+    sc = torch.exp(torch.randn((B, R + N), device="cuda", generator=g) * 1.5) * 0.02
+    sc[:, :R] = 0.3
+    sc = sc.reshape(-1).contiguous()
+    p = occam.Problem(B, 16, 16, 64, R, cands=N, dtype="bf16")
+    ws = occam.workspace(p)
+    out = torch.empty(2, dtype=torch.float32, device="cuda")
+    occam.match_lambda(p, sc, 576.0, out[0:1], ws, mean_kept=out[1:2])
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(reps):
+        occam.match_lambda(p, sc, 576.0, out[0:1], ws, mean_kept=out[1:2])
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / reps
+    lam, kept = out.cpu().tolist()
+    return {"workload": "calibration set B=%d x %d candidates, K_tar=576" % (B, N),
+            "us": round(ms * 1e3, 2), "lambda": lam, "mean_kept": kept,
+            "ratios_per_us": round(B * N / (ms * 1e3), 1)}
+
+
 def score_source_sha256() -> str:
     """sha256 of the sources the Stage II scoring kernel is built from."""
     import hashlib
@@ -364,6 +394,8 @@ def main():
         rec["cpu_baseline"] = cpu_baseline(name, lam1, lam2)
     rec["register_redirect"] = register_redirect_bench(torch)
     log("register redirect: %.1f us" % rec["register_redirect"]["us"])
+    rec["budget_matching"] = budget_matching_bench(torch)
+    log("budget matching: %.1f us" % rec["budget_matching"]["us"])
     if not args.no_mutual:
         del dv, dt
         torch.cuda.empty_cache()

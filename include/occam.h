@@ -198,6 +198,25 @@ occam_status occam_prune(const occam_problem *problem, const void *q, const void
                          int32_t *kept_offsets, void *workspace, size_t ws_bytes,
                          hipStream_t stream);
 
+/* Budget matching (Appendix Eq. lambda2_budget_matching_appendix) over the batch
+ * as the calibration set: the mean kept count (1/B) sum_b |{v : s_b(v) >= lambda *
+ * s_b(r)}| is a step function of lambda that changes at the ratios s_b(v) / s_b(r)
+ * (s_b(r) reduced from the register scores as in occam_threshold).  Among its
+ * levels the one closest to k_target wins (ties: the smaller count, i.e. the
+ * larger lambda) and lambda[0] receives the geometric midpoint of that level's
+ * interval (the level's ratio and the next smaller distinct ratio; half the ratio
+ * if there is no positive one), so that rounding lambda cannot move the count.
+ * scores: device f32 in the layout occam_score writes.  lambda, mean_kept
+ * (nullable): one device f32 each; mean_kept[0] receives the matched mean count.
+ * A batch without candidates gives lambda 1.  Ratios are formed in float32; every
+ * s_b(r) must be positive.  k_target finite >= 0.  The selection state lives in the
+ * workspace of the problem and is cleared by each call, so calls that share a
+ * workspace must be ordered on one stream. */
+occam_status occam_match_lambda(const occam_problem *problem, const float *scores,
+                                int32_t reduce, float k_target, float *lambda,
+                                float *mean_kept, void *workspace, size_t ws_bytes,
+                                hipStream_t stream);
+
 /* Test-time register construction (Algorithm 1, "redirect sinks to r"; Appendix
  * Eq. register_redirect_appendix), applied to an MLP activation tensor of the
  * vision encoder before Stage I.  For every sample b and every listed channel k:

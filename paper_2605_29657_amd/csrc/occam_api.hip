@@ -20,7 +20,7 @@ struct Plan {
     int bf16;
     int text;          // 1: several anchor rows (MFMA path); 0: one anchor row (VALU path)
     int kpw;           // keys per workgroup of the one-row path
-    size_t off_logits, off_stats, off_lse2, off_scores, off_tau, off_slot, total;
+    size_t off_logits, off_stats, off_lse2, off_scores, off_tau, off_slot, off_match, total;
 };
 
 bool aligned(const void* ptr, size_t a) { return (reinterpret_cast<uintptr_t>(ptr) % a) == 0; }
@@ -84,6 +84,7 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
     P.off_scores = off; off = align_up(off + (size_t)keys_cap * sizeof(float));
     P.off_tau = off; off = align_up(off + (size_t)B * sizeof(float));
     P.off_slot = off; off = align_up(off + (size_t)B * max_cands * sizeof(int));
+    P.off_match = off; off = align_up(off + kMatchStateBytes);
     P.total = off;
     *pl = P;
     return OCCAM_OK;
@@ -279,6 +280,22 @@ occam_status occam_prune(const occam_problem* problem, const void* q, const void
     if (st != OCCAM_OK) return st;
     return hip_ok(launch_pack_gather(P.p, slot, kept_count, index_map, kept_idx, kept_offsets,
                                      nullptr, nullptr, rows, stream));
+}
+
+occam_status occam_match_lambda(const occam_problem* problem, const float* scores, int32_t reduce,
+                                float k_target, float* lambda, float* mean_kept, void* workspace,
+                                size_t ws_bytes, hipStream_t stream) {
+    Plan P;
+    occam_status st = make_plan(problem, &P);
+    if (st != OCCAM_OK) return st;
+    if (!scores || !aligned(scores, 4) || !lambda || !aligned(lambda, 4) ||
+        (mean_kept && !aligned(mean_kept, 4)) || !reduce_ok(reduce) || !(k_target >= 0.f) ||
+        isinf(k_target))
+        return OCCAM_ERR_INVALID_ARG;
+    if ((st = check_ws(P, workspace, ws_bytes)) != OCCAM_OK) return st;
+    return hip_ok(launch_match_lambda(P.p, scores, reduce, k_target,
+                                      ws_at<char>(workspace, P.off_match), lambda, mean_kept,
+                                      stream));
 }
 
 occam_status occam_register_redirect(const occam_problem* problem, void* h, int32_t width,

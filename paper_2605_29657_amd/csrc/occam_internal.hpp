@@ -48,6 +48,18 @@ __device__ __forceinline__ int cand_begin(const Prob& p, int b) {
     return k_begin(p, b) - p.R * b;
 }
 
+// s_b(r): the register scores of one sample reduced by mean, max or sum.
+__device__ __forceinline__ float reg_reduce(const float* s, int R, int reduce) {
+    if (reduce == 1) {                     // OCCAM_REG_MAX
+        float m = s[0];
+        for (int r = 1; r < R; ++r) m = fmaxf(m, s[r]);
+        return m;
+    }
+    float acc = 0.f;
+    for (int r = 0; r < R; ++r) acc += s[r];
+    return reduce == 0 ? acc / (float)R : acc;   // MEAN : SUM
+}
+
 // bf16 <-> f32 on raw 16-bit patterns.
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -133,6 +145,10 @@ inline int cls_keys_per_wg(int H, int Hkv, int d, int elem_bytes) {
 
 // ---------------------------------------------------------------------------
 // Launchers (defined in the .hip files).  All return hipGetLastError().
+// Selection state of budget matching, in the workspace.
+constexpr size_t kMatchStateBytes = 8192;
+hipError_t launch_match_lambda(const Prob& p, const float* scores, int reduce, float k_target,
+                               void* state, float* lambda, float* mean_kept, hipStream_t s);
 hipError_t launch_register_redirect(const Prob& p, int bf16, void* h, int width, long long stride,
                                     const int* channels, int n_channels, int reg_slot,
                                     hipStream_t s);

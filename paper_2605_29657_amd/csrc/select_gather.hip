@@ -19,17 +19,6 @@
 
 namespace occam {
 
-__device__ __forceinline__ float reg_reduce(const float* s, int R, int reduce) {
-    if (reduce == 1) {                     // OCCAM_REG_MAX
-        float m = s[0];
-        for (int r = 1; r < R; ++r) m = fmaxf(m, s[r]);
-        return m;
-    }
-    float acc = 0.f;
-    for (int r = 0; r < R; ++r) acc += s[r];
-    return reduce == 0 ? acc / (float)R : acc;   // MEAN : SUM
-}
-
 __global__ void threshold_kernel(Prob p, const float* __restrict__ scores, float lambda,
                                  int reduce, float* __restrict__ tau)
 {

@@ -27,7 +27,7 @@ MAX_ROW_TENSORS = 8
 
 EXPORTS = ("occam_status_string", "occam_version", "occam_workspace_size", "occam_score",
            "occam_threshold", "occam_select", "occam_gather", "occam_prune",
-           "occam_register_redirect")
+           "occam_register_redirect", "occam_match_lambda")
 
 
 class OccamError(RuntimeError):
@@ -85,6 +85,8 @@ def lib():
         L.occam_prune.restype = i32
         L.occam_register_redirect.argtypes = [P, vp, i32, ctypes.c_int64, vp, i32, i32, vp]
         L.occam_register_redirect.restype = i32
+        L.occam_match_lambda.argtypes = [P, vp, i32, f32, vp, vp, vp, sz, vp]
+        L.occam_match_lambda.restype = i32
         _lib = L
     return _lib
 
@@ -197,6 +199,14 @@ def prune(problem, q, k, lam, kept_idx, kept_count, kept_offsets, ws, reduce=REG
                              _ptr(index_map), n, arr, _ptr(scores), _ptr(tau), _ptr(kept_idx),
                              _ptr(kept_count), _ptr(kept_offsets), _ptr(ws),
                              0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def match_lambda(problem, scores, k_target, lam_out, ws, mean_kept=None, reduce=REG_MEAN,
+                 stream=None):
+    """occam_match_lambda: writes the budget-matched lambda into ``lam_out[0]``."""
+    _check(lib().occam_match_lambda(problem.ref, _ptr(scores), int(reduce), float(k_target),
+                                    _ptr(lam_out), _ptr(mean_kept), _ptr(ws),
+                                    0 if ws is None else ws.numel(), _stream(stream)))
 
 
 def register_redirect(problem, h, channels, reg_slot=0, stream=None):

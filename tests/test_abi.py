@@ -202,3 +202,22 @@ def test_register_redirect_validation(L):
     assert L.occam_register_redirect(None, FAKE, 64, 128, FAKE, 4, 0, None) == occam.ERR_INVALID_ARG
     # n = 0 launches nothing and succeeds, even without a channel list or a GPU.
     assert call(ch=None, n=0) == occam.OK
+
+
+def test_match_lambda_validation(L):
+    p = good_problem()
+    n = occam.workspace_size(p)
+    ok = dict(sc=FAKE, red=occam.REG_MEAN, k=64.0, lam=FAKE, mk=FAKE, ws=FAKE, n=n)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return L.occam_match_lambda(p.ref, a["sc"], a["red"], a["k"], a["lam"], a["mk"], a["ws"],
+                                    a["n"], None)
+    for bad in (dict(sc=None), dict(sc=FAKE + 2), dict(red=7), dict(k=-1.0), dict(k=float("nan")),
+                dict(k=float("inf")), dict(lam=None), dict(lam=FAKE + 1), dict(mk=FAKE + 3)):
+        assert call(**bad) == occam.ERR_INVALID_ARG, bad
+    assert call(n=n - 1) == occam.ERR_WORKSPACE
+    assert call(ws=None) == occam.ERR_INVALID_ARG
+    assert L.occam_match_lambda(None, FAKE, 0, 1.0, FAKE, None, FAKE, n, None) == \
+        occam.ERR_INVALID_ARG
