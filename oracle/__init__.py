@@ -35,6 +35,7 @@ _lib = None
 _lock = threading.Lock()
 
 REG_MEAN, REG_MAX, REG_SUM = 0, 1, 2
+CAND_MEAN = 3                   # ablation: reference = mean visual score instead of s(r)
 ROWS_MAX, ROWS_MEAN = 0, 1      # visual keys: max over anchor rows (Stage II) or mean (mutual)
 _DTYPES = {"f32": 0, "bf16": 1}
 
@@ -64,6 +65,8 @@ def _load():
             lib.oracle_threshold.restype = i32
             lib.oracle_select.argtypes = [i32, i32, p, p, p, p, p, p, p]
             lib.oracle_select.restype = i32
+            lib.oracle_select_topk.argtypes = [i32, i32, p, p, i64, p, p, p, p]
+            lib.oracle_select_topk.restype = i32
             lib.oracle_gather.argtypes = [i32, i32, p, p, i64, i64, i64, p, i64, i64, p, p]
             lib.oracle_gather.restype = i32
             lib.oracle_register_redirect.argtypes = [i32, i32, p, i32, p, i64, i64, p, i32, i32]
@@ -128,7 +131,9 @@ def scores(q, k, q_off, k_off, H: int, Hkv: int, d: int, R: int, dtype: str = "b
 
 
 def threshold(sc, k_off, R: int, lam: float, reduce: int = REG_MEAN) -> np.ndarray:
-    """tau_b = lambda * s_b(r) (Eqs. stage1_threshold_appendix / stage2_set_appendix)."""
+    """tau_b = lambda * s_b(r) (Eqs. stage1_threshold_appendix / stage2_set_appendix);
+    with ``reduce=CAND_MEAN`` the ablation's mean-based threshold, lambda times the mean
+    visual score (Table tab:qwen_compact_component_ablation)."""
     lib = _load()
     k_off = _offsets(k_off)
     B = len(k_off) - 1
@@ -156,6 +161,26 @@ def select(sc, tau, k_off, R: int, index_map=None):
                            _ptr(kept), _ptr(cnt), _ptr(offs))
     if rc != 0:
         raise ValueError("oracle_select rejected the problem (rc=%d)" % rc)
+    return kept[:offs[-1]].copy(), cnt, offs
+
+
+def select_topk(sc, k_off, R: int, K: int, index_map=None):
+    """Fixed-budget ablation (Table tab:qwen_compact_component_ablation): the K highest
+    scores of each sample, lower index first among equal scores, listed ascending and
+    packed: (kept_idx, count, offsets)."""
+    lib = _load()
+    k_off = _offsets(k_off)
+    B = len(k_off) - 1
+    sc = np.ascontiguousarray(sc, dtype=np.float64)
+    ncand = int(k_off[-1] - R * B)
+    im = None if index_map is None else np.ascontiguousarray(index_map, dtype=np.int32)
+    kept = np.full(max(ncand, 1), -1, dtype=np.int32)
+    cnt = np.zeros(B, dtype=np.int32)
+    offs = np.zeros(B + 1, dtype=np.int32)
+    rc = lib.oracle_select_topk(B, R, _ptr(k_off), _ptr(sc), int(K), _ptr(im), _ptr(kept),
+                                _ptr(cnt), _ptr(offs))
+    if rc != 0:
+        raise ValueError("oracle_select_topk rejected the problem (rc=%d)" % rc)
     return kept[:offs[-1]].copy(), cnt, offs
 
 

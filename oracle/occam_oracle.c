@@ -28,6 +28,11 @@
  *   6. ascending list of survivors per sample, packed over the batch, and a
  *      byte copy of their rows (the pruned sequence [S; T] of Algorithm 1)
  *
+ * and the two threshold variants of the component ablation (Appendix, Table
+ * tab:qwen_compact_component_ablation): a mean-based threshold, lambda times
+ * the mean score of the sample's visual tokens, and a fixed budget, the K
+ * highest-scoring visual tokens of every sample.
+ *
  * Readings where the paper is silent (all listed in the design notes):
  *   - several registers: s(r) is the mean over the R register scores (MAX and
  *     SUM are offered as alternatives);
@@ -54,6 +59,7 @@
 #define ORACLE_REG_MEAN 0
 #define ORACLE_REG_MAX 1
 #define ORACLE_REG_SUM 2
+#define ORACLE_REF_CAND_MEAN 3   /* mean over the visual tokens (the ablation's mean threshold) */
 #define ORACLE_ROWS_MAX 0
 #define ORACLE_ROWS_MEAN 1
 
@@ -185,12 +191,22 @@ int oracle_threshold(int B, int R, const int64_t *k_off, const double *scores,
 {
     if (B < 0 || R < 1 || !(lambda >= 0.0) || isinf(lambda))
         return -1;
-    if (reduce != ORACLE_REG_MEAN && reduce != ORACLE_REG_MAX && reduce != ORACLE_REG_SUM)
+    if (reduce != ORACLE_REG_MEAN && reduce != ORACLE_REG_MAX && reduce != ORACLE_REG_SUM &&
+        reduce != ORACLE_REF_CAND_MEAN)
         return -1;
     for (int b = 0; b < B; ++b) {
         const double *reg = scores + k_off[b];
         double sr;
-        if (reduce == ORACLE_REG_MAX) {
+        if (reduce == ORACLE_REF_CAND_MEAN) {
+            /* Mean-based threshold: the reference is the mean visual score (0 without
+             * visual tokens, where no decision is taken). */
+            const int64_t N = k_off[b + 1] - k_off[b] - R;
+            sr = 0.0;
+            for (int64_t v = 0; v < N; ++v)
+                sr += reg[R + v];
+            if (N > 0)
+                sr /= (double)N;
+        } else if (reduce == ORACLE_REG_MAX) {
             sr = reg[0];
             for (int r = 1; r < R; ++r)
                 if (reg[r] > sr) sr = reg[r];
@@ -226,6 +242,43 @@ int oracle_select(int B, int R, const int64_t *k_off, const double *scores,
         int32_t cnt = 0;
         for (int64_t v = 0; v < N; ++v) {
             if (scores[k_off[b] + R + v] >= tau[b]) {
+                kept_idx[pos + cnt] = index_map ? index_map[co + v] : (int32_t)v;
+                ++cnt;
+            }
+        }
+        kept_count[b] = cnt;
+        pos += cnt;
+        kept_offsets[b + 1] = pos;
+    }
+    return 0;
+}
+
+/*
+ * Fixed-budget variant of step 5: keep the K visual tokens of each sample with
+ * the largest scores (all of them when N_b <= K).  Among equal scores the lower
+ * index ranks first, so the kept set is unique.  The rank of v is the number of
+ * visual tokens that come before it in that order; v is kept iff its rank is
+ * below K.  Output as in oracle_select.
+ */
+int oracle_select_topk(int B, int R, const int64_t *k_off, const double *scores, int64_t K,
+                       const int32_t *index_map, int32_t *kept_idx, int32_t *kept_count,
+                       int32_t *kept_offsets)
+{
+    if (B < 0 || R < 1 || K < 0)
+        return -1;
+    int32_t pos = 0;
+    kept_offsets[0] = 0;
+    for (int b = 0; b < B; ++b) {
+        const double *sv = scores + k_off[b] + R;
+        const int64_t N = k_off[b + 1] - k_off[b] - R;
+        const int64_t co = k_off[b] - (int64_t)R * b;
+        int32_t cnt = 0;
+        for (int64_t v = 0; v < N; ++v) {
+            int64_t rank = 0;
+            for (int64_t u = 0; u < N; ++u)
+                if (sv[u] > sv[v] || (sv[u] == sv[v] && u < v))
+                    ++rank;
+            if (rank < K) {
                 kept_idx[pos + cnt] = index_map ? index_map[co + v] : (int32_t)v;
                 ++cnt;
             }

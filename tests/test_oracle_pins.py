@@ -649,3 +649,84 @@ def test_register_redirect_absorbs_a_sink_channel():
     out = oracle.register_redirect(h, k_off, R, [9], dtype="f32")
     assert out[0, 9] == 80.0 and np.max(np.abs(out[R:, 9])) == 0.0
     assert np.linalg.norm(out[R + 11]) < 0.5 * np.linalg.norm(h[R + 11])
+
+
+def test_budget_matching_tie_rule_and_interval_ends():
+    # Ratios 1..4 of one sample: counts 4, 3, 2, 1 at 1, 2, 3, 4.  A target of 2.5 is
+    # equally far from 2 and 3: the smaller count wins, lambda = sqrt(3 * 2).
+    assert oracle.match_lambda([np.array([1.0, 2.0, 3.0, 4.0])], 2.5) == pytest.approx(np.sqrt(6))
+    # Beyond every candidate: the lowest level, half its ratio (no ratio below it).
+    assert oracle.match_lambda([np.array([1.0, 2.0, 3.0, 4.0])], 100.0) == 0.5
+    # Two samples: the mean count is halved; target 1 = count 2 over the batch.
+    lam = oracle.match_lambda([np.array([4.0, 1.0]), np.array([3.0, 2.0])], 1.0)
+    assert lam == pytest.approx(np.sqrt(3 * 2))
+    assert oracle.match_lambda([np.zeros(0)], 3.0) == 1.0
+
+
+# ----------------------------------------------------------------------------- ablation
+def test_mean_threshold_hand_example_and_invariants():
+    # Table tab:qwen_compact_component_ablation, mean-based threshold: tau = lambda * mean
+    # of the visual scores; the register scores do not enter.
+    sc = np.array([0.1, 0.2, 0.3, 0.1, 0.3, 0.05, 0.9, 0.4, 0.4, 0.4])
+    k_off = [0, 6, 10]
+    tau = oracle.threshold(sc, k_off, 2, 1.0, oracle.CAND_MEAN)
+    assert tau[0] == pytest.approx(0.75 / 4) and tau[1] == pytest.approx(0.4)
+    rng = np.random.default_rng(41)
+    R, N = 3, 200
+    s = rng.random(R + N)
+    t1 = oracle.threshold(s, [0, R + N], R, 1.3, oracle.CAND_MEAN)
+    s2 = s.copy()
+    s2[:R] = rng.random(R) * 50                        # registers changed: same threshold
+    assert oracle.threshold(s2, [0, R + N], R, 1.3, oracle.CAND_MEAN)[0] == t1[0]
+    # Scale invariance of the decisions, and lambda = 1 keeps some but not all tokens.
+    kept1 = oracle.select(s, t1, [0, R + N], R)[0]
+    t3 = oracle.threshold(s * 8.0, [0, R + N], R, 1.3, oracle.CAND_MEAN)
+    assert np.array_equal(oracle.select(s * 8.0, t3, [0, R + N], R)[0], kept1)
+    t_one = oracle.threshold(s, [0, R + N], R, 1.0, oracle.CAND_MEAN)
+    n_one = len(oracle.select(s, t_one, [0, R + N], R)[0])
+    assert 0 < n_one < N
+    # Uniform visual scores: lambda = 1 keeps all, anything above keeps none.
+    u = np.concatenate([s[:R], np.full(N, 0.125)])
+    for lam, want in ((1.0, N), (1.0 + 1e-12, 0)):
+        t = oracle.threshold(u, [0, R + N], R, lam, oracle.CAND_MEAN)
+        assert len(oracle.select(u, t, [0, R + N], R)[0]) == want
+    # No visual tokens: tau = 0, nothing to keep.
+    assert oracle.threshold(s[:R], [0, R], R, 2.0, oracle.CAND_MEAN)[0] == 0.0
+
+
+def test_topk_is_the_sorted_prefix():
+    # Fixed budget: the K best by (score desc, index asc), i.e. numpy's stable lexsort.
+    rng = np.random.default_rng(43)
+    R = 2
+    N = np.array([0, 1, 7, 40, 300])
+    k_off = np.concatenate([[0], np.cumsum(N + R)])
+    sc = np.round(rng.random(int(k_off[-1])) * 16) / 16   # many ties
+    for K in (0, 1, 5, 40, 1000):
+        kept, cnt, offs = oracle.select_topk(sc, k_off, R, K)
+        for b in range(len(N)):
+            sv = sc[k_off[b] + R:k_off[b + 1]]
+            order = np.lexsort((np.arange(N[b]), -sv))       # last key sorts first
+            want = np.sort(order[:K])
+            got = kept[offs[b]:offs[b + 1]]
+            assert np.array_equal(got, want), (b, K)
+            assert cnt[b] == min(K, N[b])
+            # Every kept token beats every dropped one (or ties with a lower index).
+            drop = np.setdiff1d(np.arange(N[b]), got)
+            for v in got:
+                assert np.all((sv[v] > sv[drop]) | ((sv[v] == sv[drop]) & (v < drop)))
+
+
+def test_topk_matches_the_threshold_rule_without_ties_and_maps_indices():
+    # With distinct scores, keeping the K best equals the threshold rule at the K-th
+    # largest score; index_map entries replace the local indices.
+    rng = np.random.default_rng(47)
+    R, N = 1, 500
+    sc = rng.random(R + N)
+    for K in (1, 17, 250, 499):
+        kth = np.sort(sc[R:])[::-1][K - 1]
+        kept_t = oracle.select(sc, np.array([kth]), [0, R + N], R)[0]
+        assert np.array_equal(oracle.select_topk(sc, [0, R + N], R, K)[0], kept_t)
+    im = (np.arange(N) * 7 + 3).astype(np.int32)
+    kept, _, _ = oracle.select_topk(sc, [0, R + N], R, 10)
+    kept_m, _, _ = oracle.select_topk(sc, [0, R + N], R, 10, index_map=im)
+    assert np.array_equal(kept_m, im[kept])
