@@ -194,6 +194,73 @@ def budget_matching_bench(torch, reps: int = 20) -> dict:
             "ratios_per_us": round(B * N / (ms * 1e3), 1)}
 
 
+def ablation_steps(torch, dv, dt, k1: float, k2: float, steps: int) -> dict:
+    """The component ablation's two threshold variants (Table
+    tab:qwen_compact_component_ablation) on the headline batch, each at the register
+    rule's mean budgets k1 / k2 (the paper compares variants at matched retention):
+
+    * mean threshold: lambda matched on the device (occam_match_lambda with the mean
+      visual score as reference) to k1 / k2, then the same fused prune of both stages;
+    * fixed budget: occam_score, occam_select_topk with K = round(k1) / round(k2), and
+      occam_gather of the same rows.
+    """
+    from paper_2605_29657_amd import occam
+    lam = torch.empty(2, dtype=torch.float32, device="cuda")
+    mk = torch.empty(2, dtype=torch.float32, device="cuda")
+    for i, (ds, k) in enumerate(((dv, k1), (dt, k2))):
+        occam.score(ds.problem, ds.q, ds.k, ds.out["scores"], ds.ws)
+        occam.match_lambda(ds.problem, ds.out["scores"], k, lam[i:i + 1], ds.ws,
+                           mean_kept=mk[i:i + 1], reduce=occam.REF_CAND_MEAN)
+    lam1, lam2 = lam.cpu().tolist()
+    K1, K2 = int(round(k1)), int(round(k2))
+
+    def mean_step():
+        dv.prune(lam1, reduce=occam.REF_CAND_MEAN)
+        dt.prune(lam2, reduce=occam.REF_CAND_MEAN)
+
+    def topk(ds, K):
+        o = ds.out
+        occam.score(ds.problem, ds.q, ds.k, o["scores"], ds.ws)
+        occam.select_topk(ds.problem, o["scores"], K, o["kept_idx"], o["kept_count"],
+                          o["kept_offsets"], ds.ws)
+        occam.gather(ds.problem, ds.rows, o["kept_idx"], o["kept_offsets"])
+
+    def topk_step():
+        topk(dv, K1)
+        topk(dt, K2)
+
+    def timed(fn, n):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    B = dv.sb.B
+    ms_mean = timed(mean_step, steps)
+    kept_mean = (float(dv.out["kept_count"].float().mean()), float(dt.out["kept_count"].float().mean()))
+    ms_topk = timed(topk_step, steps)
+    sel_us = timed(lambda: occam.select_topk(dt.problem, dt.out["scores"], K2, dt.out["kept_idx"],
+                                             dt.out["kept_count"], dt.out["kept_offsets"], dt.ws),
+                   steps) * 1e3
+    thr_us = timed(lambda: occam.select(dt.problem, dt.out["scores"], dt.out["tau"],
+                                        dt.out["kept_idx"], dt.out["kept_count"],
+                                        dt.out["kept_offsets"], dt.ws), steps) * 1e3
+    return {"mean_threshold": {"lambda1": lam1, "lambda2": lam2,
+                               "kept_stage1_mean": kept_mean[0], "kept_stage2_mean": kept_mean[1],
+                               "ms_per_step": round(ms_mean, 4),
+                               "images_s": round(B / (ms_mean * 1e-3), 1)},
+            "fixed_budget": {"K1": K1, "K2": K2, "ms_per_step": round(ms_topk, 4),
+                             "images_s": round(B / (ms_topk * 1e-3), 1),
+                             "select_topk_stage2_us": round(sel_us, 2),
+                             "select_threshold_stage2_us": round(thr_us, 2)}}
+
+
 def score_source_sha256() -> str:
     """sha256 of the sources the Stage II scoring kernel is built from."""
     import hashlib
@@ -396,6 +463,11 @@ def main():
     log("register redirect: %.1f us" % rec["register_redirect"]["us"])
     rec["budget_matching"] = budget_matching_bench(torch)
     log("budget matching: %.1f us" % rec["budget_matching"]["us"])
+    rec["ablation"] = ablation_steps(torch, dv, dt, float(kept1.mean()), float(kept2.mean()),
+                                     max(10, args.steps // 2))
+    log("ablation: mean threshold %.3f ms/step, fixed budget %.3f ms/step" % (
+        rec["ablation"]["mean_threshold"]["ms_per_step"],
+        rec["ablation"]["fixed_budget"]["ms_per_step"]))
     if not args.no_mutual:
         del dv, dt
         torch.cuda.empty_cache()

@@ -92,8 +92,16 @@ typedef enum { OCCAM_F32 = 0, OCCAM_BF16 = 1 } occam_dtype;
 
 /* How the R register scores are combined into s(r).  The paper builds one
  * register (Appendix, "Parameter settings"); with several, MEAN is the default
- * reading and equals the paper's rule at R = 1. */
-typedef enum { OCCAM_REG_MEAN = 0, OCCAM_REG_MAX = 1, OCCAM_REG_SUM = 2 } occam_reg_reduce;
+ * reading and equals the paper's rule at R = 1.  CAND_MEAN replaces s(r) by the
+ * mean score of the sample's visual tokens (0 when it has none): the mean-based
+ * threshold of the component ablation (Appendix, Table
+ * tab:qwen_compact_component_ablation). */
+typedef enum {
+    OCCAM_REG_MEAN = 0,
+    OCCAM_REG_MAX = 1,
+    OCCAM_REG_SUM = 2,
+    OCCAM_REF_CAND_MEAN = 3
+} occam_reg_reduce;
 
 /* How a visual key's score is reduced over the anchor rows (registers always take
  * the mean).  MAX: the text rows of Stage II (Sec. 3.5, Eq. text_scoring).  MEAN:
@@ -179,6 +187,16 @@ occam_status occam_select(const occam_problem *problem, const float *scores, con
                           const int32_t *index_map, int32_t *kept_idx, int32_t *kept_count,
                           int32_t *kept_offsets, void *workspace, size_t ws_bytes,
                           hipStream_t stream);
+
+/* Fixed-budget variant of steps 4-5 (the component ablation, Appendix Table
+ * tab:qwen_compact_component_ablation): keep the min(k_keep, N_b) visual tokens
+ * of each sample with the largest scores; among equal scores the lower index
+ * ranks first, so the kept set is unique.  Output exactly as occam_select
+ * (ascending, packed, counts, offsets, index_map).  k_keep >= 0. */
+occam_status occam_select_topk(const occam_problem *problem, const float *scores,
+                               int32_t k_keep, const int32_t *index_map, int32_t *kept_idx,
+                               int32_t *kept_count, int32_t *kept_offsets, void *workspace,
+                               size_t ws_bytes, hipStream_t stream);
 
 /* Step 5, materialisation (Algorithm 1, the pruned sequence): for each of
  * the n row tensors, copy the row of every listed survivor, byte for byte, to

@@ -19,12 +19,13 @@
 //                the rank left inside it.
 //   match_count  same grid: #{key >= v1}, #{key > v1}, the nearest keys above and
 //                below v1; the last workgroup chooses the level and writes lambda.
-// Every workgroup recomputes s_b(r) for its own sample from the register scores.
+// Every workgroup recomputes its sample's reference (s_b(r), or the mean visual score
+// of the ablation) with the same reduction as the threshold kernels.
 #include "occam_internal.hpp"
 
 namespace occam {
 
-constexpr int kMatchThreads = 256;
+constexpr int kMatchThreads = kSelThreads;      // same reference bits as occam_threshold
 constexpr int kMatchPer = 4;                              // keys per thread per chunk
 constexpr int kMatchChunk = kMatchThreads * kMatchPer;
 
@@ -38,13 +39,6 @@ struct MatchState {
 };
 static_assert(sizeof(MatchState) <= kMatchStateBytes, "match state exceeds its workspace");
 
-__device__ __forceinline__ uint32_t order_key(float r) {
-    const uint32_t u = r == 0.f ? 0u : __float_as_uint(r);       // -0 folds into +0
-    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__device__ __forceinline__ float key_value(uint32_t k) {
-    return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
-}
 __device__ __forceinline__ uint32_t load_cc(const uint32_t* a) {  // coherent across workgroups
     return __hip_atomic_load(a, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -55,10 +49,11 @@ struct ChunkKeys {
     bool valid[kMatchPer];
 };
 __device__ __forceinline__ ChunkKeys chunk_keys(const Prob& p, const float* scores, int reduce) {
+    __shared__ float red[kMatchThreads / kWave];
     const int b = blockIdx.x;
     const int kb = k_begin(p, b);
     const int N = keys_of(p, b) - p.R;
-    const float sr = reg_reduce(scores + kb, p.R, reduce);
+    const float sr = sample_reference<kMatchThreads>(p, scores, b, reduce, red);
     ChunkKeys ck;
 #pragma unroll
     for (int j = 0; j < kMatchPer; ++j) {

@@ -100,7 +100,10 @@ occam_status check_ws(const Plan& P, void* ws, size_t ws_bytes) {
 }
 
 bool lambda_ok(float lambda) { return lambda >= 0.f && !isinf(lambda); }
-bool reduce_ok(int32_t r) { return r == OCCAM_REG_MEAN || r == OCCAM_REG_MAX || r == OCCAM_REG_SUM; }
+bool reduce_ok(int32_t r) {
+    return r == OCCAM_REG_MEAN || r == OCCAM_REG_MAX || r == OCCAM_REG_SUM ||
+           r == OCCAM_REF_CAND_MEAN;
+}
 
 occam_status rows_from(int32_t n, const occam_rows* t, RowTensors* out) {
     memset(out, 0, sizeof *out);
@@ -232,6 +235,27 @@ occam_status occam_select(const occam_problem* problem, const float* scores, con
     if ((st = check_ws(P, workspace, ws_bytes)) != OCCAM_OK) return st;
     int* slot = ws_at<int>(workspace, P.off_slot);
     st = hip_ok(launch_select(P.p, scores, tau, 0, 0.f, 0, nullptr, slot, kept_count, stream));
+    if (st != OCCAM_OK) return st;
+    RowTensors none;
+    memset(&none, 0, sizeof none);
+    return hip_ok(launch_pack_gather(P.p, slot, kept_count, index_map, kept_idx, kept_offsets,
+                                     nullptr, nullptr, none, stream));
+}
+
+occam_status occam_select_topk(const occam_problem* problem, const float* scores, int32_t k_keep,
+                               const int32_t* index_map, int32_t* kept_idx, int32_t* kept_count,
+                               int32_t* kept_offsets, void* workspace, size_t ws_bytes,
+                               hipStream_t stream) {
+    Plan P;
+    occam_status st = make_plan(problem, &P);
+    if (st != OCCAM_OK) return st;
+    if (!scores || !kept_idx || !kept_count || !kept_offsets || !aligned(scores, 4) ||
+        !aligned(kept_idx, 4) || !aligned(kept_count, 4) || !aligned(kept_offsets, 4) ||
+        (index_map && !aligned(index_map, 4)) || k_keep < 0)
+        return OCCAM_ERR_INVALID_ARG;
+    if ((st = check_ws(P, workspace, ws_bytes)) != OCCAM_OK) return st;
+    int* slot = ws_at<int>(workspace, P.off_slot);
+    st = hip_ok(launch_select_topk(P.p, scores, k_keep, slot, kept_count, stream));
     if (st != OCCAM_OK) return st;
     RowTensors none;
     memset(&none, 0, sizeof none);

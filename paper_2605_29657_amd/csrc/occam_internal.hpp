@@ -60,6 +60,43 @@ __device__ __forceinline__ float reg_reduce(const float* s, int R, int reduce) {
     return reduce == 0 ? acc / (float)R : acc;   // MEAN : SUM
 }
 
+constexpr int kRefCandMean = 3;            // OCCAM_REF_CAND_MEAN
+
+// Reference score of sample b, returned to every thread of a workgroup of NT threads
+// (all of them must call it).  Register reductions read the R register scores; the
+// candidate mean sums the visual scores in a fixed order (strided per thread, a fixed
+// shuffle tree per wave, the waves in order), so every kernel that calls it with the
+// same NT gets the same bits.  `red` is NT / 64 floats of LDS.
+template <int NT>
+__device__ __forceinline__ float sample_reference(const Prob& p, const float* scores, int b,
+                                                  int reduce, float* red) {
+    const int kb = k_begin(p, b);
+    if (reduce != kRefCandMean) return reg_reduce(scores + kb, p.R, reduce);
+    const int N = keys_of(p, b) - p.R;
+    const float* sv = scores + kb + p.R;
+    float acc = 0.f;
+    for (int v = threadIdx.x; v < N; v += NT) acc += sv[v];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
+    __syncthreads();                          // `red` may still be read by a previous call
+    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+    __syncthreads();
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < NT / 64; ++w) sum += red[w];
+    return N > 0 ? sum / (float)N : 0.f;
+}
+
+// Floats as unsigned keys with the same order: -0 folds into +0, non-negative values
+// set the top bit, negative values are bit-inverted.
+__device__ __forceinline__ uint32_t order_key(float x) {
+    const uint32_t u = x == 0.f ? 0u : __float_as_uint(x);
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_value(uint32_t k) {
+    return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
 // bf16 <-> f32 on raw 16-bit patterns.
 __device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
@@ -145,6 +182,8 @@ inline int cls_keys_per_wg(int H, int Hkv, int d, int elem_bytes) {
 
 // ---------------------------------------------------------------------------
 // Launchers (defined in the .hip files).  All return hipGetLastError().
+hipError_t launch_select_topk(const Prob& p, const float* scores, int k_keep, int* slot,
+                              int* count, hipStream_t s);
 // Selection state of budget matching, in the workspace.
 constexpr size_t kMatchStateBytes = 8192;
 hipError_t launch_match_lambda(const Prob& p, const float* scores, int reduce, float k_target,

@@ -27,6 +27,15 @@ __global__ void threshold_kernel(Prob p, const float* __restrict__ scores, float
     tau[b] = lambda * reg_reduce(scores + k_begin(p, b), p.R, reduce);
 }
 
+// Mean-based threshold: one workgroup per sample reduces its visual scores.
+__global__ __launch_bounds__(kSelThreads) void threshold_mean_kernel(
+    Prob p, const float* __restrict__ scores, float lambda, float* __restrict__ tau)
+{
+    __shared__ float red[kSelThreads / kWave];
+    const float ref = sample_reference<kSelThreads>(p, scores, blockIdx.x, kRefCandMean, red);
+    if (threadIdx.x == 0) tau[blockIdx.x] = lambda * ref;
+}
+
 __global__ __launch_bounds__(kSelThreads) void select_kernel(
     Prob p, const float* __restrict__ scores, const float* __restrict__ tau_in, int fuse_tau,
     float lambda, int reduce, float* __restrict__ tau_out, int* __restrict__ slot,
@@ -36,21 +45,21 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
     // it counts its survivors, one block-wide exclusive scan gives every strip its
     // output position, and the strip writes its survivors in ascending order.
     __shared__ int wsum[kSelThreads / kWave];
+    __shared__ float red[kSelThreads / kWave];
     __shared__ float tau_s;
     const int b = blockIdx.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int kb = k_begin(p, b);
     const int N = keys_of(p, b) - p.R;
     const int co = cand_begin(p, b);
-    if (tid == 0) {
-        float t;
-        if (fuse_tau) {
-            t = lambda * reg_reduce(scores + kb, p.R, reduce);
+    if (fuse_tau) {
+        const float t = lambda * sample_reference<kSelThreads>(p, scores, b, reduce, red);
+        if (tid == 0) {
             if (tau_out) tau_out[b] = t;
-        } else {
-            t = tau_in[b];
+            tau_s = t;
         }
-        tau_s = t;
+    } else if (tid == 0) {
+        tau_s = tau_in[b];
     }
     __syncthreads();
     const float tau = tau_s;
@@ -154,8 +163,12 @@ __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
 hipError_t launch_threshold(const Prob& p, const float* scores, float lambda, int reduce,
                             float* tau, hipStream_t s)
 {
-    hipLaunchKernelGGL(threshold_kernel, dim3((p.B + 255) / 256), dim3(256), 0, s, p, scores,
-                       lambda, reduce, tau);
+    if (reduce == kRefCandMean)
+        hipLaunchKernelGGL(threshold_mean_kernel, dim3(p.B), dim3(kSelThreads), 0, s, p, scores,
+                           lambda, tau);
+    else
+        hipLaunchKernelGGL(threshold_kernel, dim3((p.B + 255) / 256), dim3(256), 0, s, p, scores,
+                           lambda, reduce, tau);
     return hipGetLastError();
 }
 

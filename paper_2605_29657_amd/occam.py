@@ -22,12 +22,13 @@ LIB_PATH = os.path.join(_HERE, "liboccam.so")
 OK, ERR_INVALID_ARG, ERR_UNSUPPORTED, ERR_WORKSPACE, ERR_HIP = range(5)
 F32, BF16 = 0, 1
 REG_MEAN, REG_MAX, REG_SUM = 0, 1, 2
+REF_CAND_MEAN = 3               # mean-based threshold of the component ablation
 ROWS_MAX, ROWS_MEAN = 0, 1
 MAX_ROW_TENSORS = 8
 
 EXPORTS = ("occam_status_string", "occam_version", "occam_workspace_size", "occam_score",
            "occam_threshold", "occam_select", "occam_gather", "occam_prune",
-           "occam_register_redirect", "occam_match_lambda")
+           "occam_register_redirect", "occam_match_lambda", "occam_select_topk")
 
 
 class OccamError(RuntimeError):
@@ -78,6 +79,8 @@ def lib():
         L.occam_threshold.restype = i32
         L.occam_select.argtypes = [P, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.occam_select.restype = i32
+        L.occam_select_topk.argtypes = [P, vp, i32, vp, vp, vp, vp, vp, sz, vp]
+        L.occam_select_topk.restype = i32
         L.occam_gather.argtypes = [P, i32, RP, vp, vp, vp]
         L.occam_gather.restype = i32
         L.occam_prune.argtypes = [P, vp, vp, vp, f32, i32, vp, i32, RP, vp, vp, vp, vp, vp, vp,
@@ -190,6 +193,13 @@ def gather(problem, rows, kept_idx, kept_offsets, stream=None):
     n, arr = _rows_array(rows)
     _check(lib().occam_gather(problem.ref, n, arr, _ptr(kept_idx), _ptr(kept_offsets),
                               _stream(stream)))
+
+
+def select_topk(problem, scores, k_keep, kept_idx, kept_count, kept_offsets, ws, index_map=None,
+                stream=None):
+    _check(lib().occam_select_topk(problem.ref, _ptr(scores), int(k_keep), _ptr(index_map),
+                                   _ptr(kept_idx), _ptr(kept_count), _ptr(kept_offsets),
+                                   _ptr(ws), 0 if ws is None else ws.numel(), _stream(stream)))
 
 
 def prune(problem, q, k, lam, kept_idx, kept_count, kept_offsets, ws, reduce=REG_MEAN,

@@ -143,7 +143,8 @@ def test_threshold_and_prune_reject_bad_lambda(L, lam):
 
 def test_reduce_mode_is_checked(L):
     p = good_problem()
-    assert L.occam_threshold(p.ref, FAKE, 0.5, 3, FAKE, None) == occam.ERR_INVALID_ARG
+    for bad in (4, -1, 99):
+        assert L.occam_threshold(p.ref, FAKE, 0.5, bad, FAKE, None) == occam.ERR_INVALID_ARG
 
 
 def test_select_argument_checks(L):
@@ -220,4 +221,27 @@ def test_match_lambda_validation(L):
     assert call(n=n - 1) == occam.ERR_WORKSPACE
     assert call(ws=None) == occam.ERR_INVALID_ARG
     assert L.occam_match_lambda(None, FAKE, 0, 1.0, FAKE, None, FAKE, n, None) == \
+        occam.ERR_INVALID_ARG
+
+
+def test_select_topk_validation(L):
+    p = good_problem()
+    n = occam.workspace_size(p)
+    ok = dict(sc=FAKE, k=8, im=None, idx=FAKE, cnt=FAKE, off=FAKE, ws=FAKE, n=n)
+
+    def call(**kw):
+        a = dict(ok)
+        a.update(kw)
+        return L.occam_select_topk(p.ref, a["sc"], a["k"], a["im"], a["idx"], a["cnt"], a["off"],
+                                   a["ws"], a["n"], None)
+    for bad in (dict(sc=None), dict(sc=FAKE + 2), dict(k=-1), dict(im=FAKE + 1), dict(idx=None),
+                dict(cnt=FAKE + 2), dict(off=None), dict(ws=None)):
+        assert call(**bad) == occam.ERR_INVALID_ARG, bad
+    assert call(n=n - 1) == occam.ERR_WORKSPACE
+
+
+def test_mean_threshold_is_an_accepted_reduction(L):
+    # OCCAM_REF_CAND_MEAN passes the reduction check (the null scores are what fail).
+    p = good_problem()
+    assert L.occam_threshold(p.ref, None, ctypes.c_float(1.0), occam.REF_CAND_MEAN, FAKE, None) == \
         occam.ERR_INVALID_ARG
