@@ -327,11 +327,15 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     const int wkey0 = s_lo + wave * kTxtKeysPerWave;
     const bool wactive = wkey0 < S;
     const int R = p.R;
-    // Loop step hh works on head (hh + rot) mod H, rot = workgroup id mod H: a key row's
-    // head slices all sit at the same offset within 8 KB rows, so workgroups moving
-    // through the heads in step would load the same memory channels at the same time.
-    // Steps past the last head repeat the last one (clamped prefetches).
-    const int rot = (int)(blockIdx.x % (unsigned)H);
+    // Loop step hh works on head (hh + rot) mod H: a key row's head slices all sit at
+    // the same offset within 8 KB rows, so workgroups moving through the heads in step
+    // would load the same memory channels at the same time.  Eight starting heads,
+    // spread over the H heads, balance the channels as well as H of them do, and keep
+    // at most eight of a sample's query tiles in use at once, so that the L2 of its XCD
+    // serves the other workgroups' tile reads.  Steps past the last head repeat the
+    // last one (clamped prefetches).
+    const int nrot = H < 8 ? H : 8;
+    const int rot = (int)(blockIdx.x % (unsigned)nrot) * (H / nrot);
     auto head_of = [&](int hh) {
         const int hc = min(hh, H - 1) + rot;
         return hc >= H ? hc - H : hc;
