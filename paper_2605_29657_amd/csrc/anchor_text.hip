@@ -105,11 +105,11 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     float* __restrict__ lse2)
 {
-    // 8 waves: wave w owns rows [64*(w&1), +64) of the row block and the key stream
-    // ks = w>>1 (key blocks kbi = ks (mod 4)).  The two waves of a stream consume the
-    // same key blocks, so each block is copied once per pair, global -> LDS, into a
-    // ring of kRing stages per stream: kRing - 1 blocks are in flight while one is
-    // used.  A block is 32 keys x NCH 16-byte chunks; chunk c of key j sits in LDS
+    // kStatsThreads / 64 waves: wave w owns rows [64*(w&1), +64) of the row block and
+    // the key stream ks = w>>1 (key blocks kbi = ks mod kStreams).  The two waves of a
+    // stream consume the same key blocks, so each block is copied once per pair,
+    // global -> LDS, into a ring of kStatsRing stages per stream: kStatsRing - 1 blocks
+    // are in flight while one is used.  A block is 32 keys x NCH 16-byte chunks; chunk c of key j sits in LDS
     // unit j*NCH + (c ^ (j & SW)), SW = NCH - 1 when NCH is a power of two (else 0),
     // so a copy writes whole 256-byte key slices and the MFMA fragment reads of 32
     // consecutive keys spread over the banks.

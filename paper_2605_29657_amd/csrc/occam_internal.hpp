@@ -122,7 +122,7 @@ constexpr int kClsPartials = 8192;   // LDS floats of per-chunk partial dot prod
 // Text (T > 1) path: MFMA 32x32x16 bf16; 4 waves; a t-block of 128 anchor rows
 // (4 sub-blocks of 32) and 32 keys per wave.
 constexpr int kTxtThreads = 256;
-constexpr int kStatsThreads = 512;
+constexpr int kStatsThreads = 256;
 constexpr int kScoreThreads = 256;
 constexpr int kTxtRows = 128;
 constexpr int kTxtKeysPerWave = 32;
@@ -150,8 +150,11 @@ inline size_t text_score_smem(int H, int d16) {
 }
 
 // Dynamic LDS of the text-row statistics kernel: a ring of kStatsRing key blocks
-// (32 keys x d bf16) per key stream, plus the (max, sum) merge arrays.
-constexpr int kStatsRing = 4;
+// (32 keys x d bf16) per key stream, plus the (max, sum) merge arrays.  Two stages (one
+// block in flight per stream while the other is used) and four workgroups per CU read
+// the head slices faster than deeper rings at fewer workgroups per CU: the scattered
+// 256-byte slices stream better with fewer requests outstanding per CU.
+constexpr int kStatsRing = 2;
 inline size_t text_stats_smem(int d16) {
     return (size_t)(kStatsThreads / kWave / 2) * kStatsRing * 32 * d16 * 2 +
            2 * (size_t)(kStatsThreads / kWave / 2) * kTxtRows * 4;
