@@ -100,10 +100,18 @@ __device__ __forceinline__ void wait_vmem_le() {
     __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | 0x0F70);
 }
 
-template <int DS, bool HALF>
+// COLSUM = false: the base-2 log-sum-exp of every (row, head) over the sample's keys
+// (lse2).  COLSUM = true (mutual scoring, Eq. mutual_scoring): with the normalisers
+// given (lse_in), the sum over this workgroup's 128 rows of p = 2^(x - lse2) for every
+// key, written to part[b][row block][h][key]; the mean over rows and heads is then a
+// fixed-order sum over the partials (text_colsum_reduce).  Both modes stream the keys
+// the same way; the column sums use the MFMA the other way round (rows as the A
+// operand), so that a lane holds 16 rows of one key and sums them in registers.
+template <int DS, bool HALF, bool COLSUM>
 __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-    float* __restrict__ lse2)
+    float* __restrict__ lse2, const float* __restrict__ lse_in, int lse_natural,
+    float* __restrict__ part)
 {
     // kStatsThreads / 64 waves: wave w owns rows [64*(w&1), +64) of the row block and
     // the key stream ks = w>>1 (key blocks kbi = ks mod kStreams).  The two waves of a
@@ -152,6 +160,23 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     float m[2], z[2];
 #pragma unroll
     for (int sb = 0; sb < 2; ++sb) { m[sb] = -INFINITY; z[sb] = 0.f; }
+    // COLSUM: base-2 normaliser of the 16 rows this lane holds in each sub-block (row
+    // 8*(r/4) + 4*hi + r%4 of the sub-block); rows past T_b get +inf and weigh 0.
+    float lsev[COLSUM ? 2 : 1][16];
+    if (COLSUM) {
+#pragma unroll
+        for (int sb = 0; sb < 2; ++sb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+                const int t = tw + sb * 32 + acc_key(r, hi);
+                float v = INFINITY;
+                if (t < T) {
+                    v = lse_in[(size_t)(qb + t) * H + h];
+                    if (lse_natural) v *= kLog2e;
+                }
+                lsev[sb][r] = v;
+            }
+    }
 
     const int nkb = (S + 31) >> 5;
     const int nmine = (nkb - ks + kStreams - 1) / kStreams;     // blocks of this stream
@@ -200,7 +225,7 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     const uint32_t kfrag = (uint32_t)(lo * NCH + (hi ^ (lo & SW))) * 16u;
 
     // One key block: MFMA logits from the LDS stage, then the online (max, sum) update.
-    auto block = [&](int kbi, const u32x4* blk) {
+    auto block = [&](int kbi, const u32x4* blk) -> float {
         const int nvalid = S - kbi * 32;
         u32x4 kf[DS];
 #pragma unroll
@@ -213,6 +238,23 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
         f32x16 acc[2];
 #pragma unroll
         for (int sb = 0; sb < 2; ++sb) acc[sb] = f32x16{};
+        if (COLSUM) {
+            // Rows as the A operand: lane (key lo, half hi) holds rows acc_key(r, hi).
+#pragma unroll
+            for (int kk = 0; kk < DS; ++kk) {
+                acc[0] = mfma32(qf[0][kk], as_bf16x8(kf[kk]), acc[0]);
+                if (nsb > 1) acc[1] = mfma32(qf[1][kk], as_bf16x8(kf[kk]), acc[1]);
+            }
+            float cs = 0.f;
+#pragma unroll
+            for (int sb = 0; sb < 2; ++sb) {
+                if (sb >= nsb) break;
+#pragma unroll
+                for (int r = 0; r < 16; ++r)
+                    cs += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -lsev[sb][r]));
+            }
+            return cs + __shfl_xor(cs, 32);
+        }
 #pragma unroll
         for (int kk = 0; kk < DS; ++kk) {
             acc[0] = mfma32(as_bf16x8(kf[kk]), qf[0][kk], acc[0]);
@@ -244,11 +286,23 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
             z[sb] = z[sb] * __builtin_amdgcn_exp2f(m[sb] - mn) + sum;
             m[sb] = mn;
         }
+        return 0.f;
     };
 
     // Every wave runs the same number of iterations (the most any stream has), so the
     // barriers match; a stream past its last block only re-issues its last block.
     const int iters = (nkb + kStreams - 1) / kStreams;
+    // COLSUM: the two row halves of a stream leave their column sums of block j in
+    // sums[j & 1][ks][rh][key]; after the next barrier the rh = 0 wave adds the pair (in
+    // that order) and stores the workgroup's partial.
+    float* sums = red_m;
+    float* prow = part + (((size_t)b * ((p.max_rows + kTxtRows - 1) / kTxtRows) + tblk) * H + h) *
+                             (size_t)(p.R + p.max_cands);
+    auto store_sums = [&](int j) {
+        const float* sp = sums + ((j & 1) * kStreams + ks) * 64;
+        const int key = (ks + j * kStreams) * 32 + lane;
+        if (lane < 32 && key < S) prow[key] = sp[lane] + sp[32 + lane];
+    };
 #pragma unroll
     for (int j = 0; j < kStatsRing - 1; ++j) issue(j);
     for (int i = 0; i < iters; ++i) {
@@ -257,9 +311,19 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
         else wait_vmem_le<(kStatsRing - 2) * MINE1>();
         __syncthreads();                 // partner's copies landed; stage (i-1) is free
         issue(i + kStatsRing - 1);
-        if (i < nmine && nsb > 0) block(ks + i * kStreams, sring + (i % kStatsRing) * UNITS);
+        if (COLSUM && rh == 0 && i >= 1 && i - 1 < nmine) store_sums(i - 1);
+        if (i < nmine) {
+            float cs = 0.f;
+            if (nsb > 0) cs = block(ks + i * kStreams, sring + (i % kStatsRing) * UNITS);
+            if (COLSUM && hi == 0) sums[((i & 1) * kStreams + ks) * 64 + rh * 32 + lo] = cs;
+        }
     }
     wait_vmem_le<0>();
+    if (COLSUM) {
+        __syncthreads();
+        if (rh == 0 && iters >= 1 && iters - 1 < nmine) store_sums(iters - 1);
+        return;
+    }
 
     // Merge the two lane halves (same rows, different keys), then the key streams.
 #pragma unroll
@@ -474,11 +538,10 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
         }
     }
 
-    // Row reduction of Eq. text_scoring (visual keys: max over rows) or Eq.
-    // mutual_scoring (every key: mean over rows): over the lane's sub-blocks, then
-    // across the 32 lanes of a lane half (fixed order).  Rows past T_b hold exact zeros.
-    const bool mean_rows = p.mean_rows != 0;
-    const bool regs = wactive && (mean_rows || wkey0 < R);   // keys whose row sum is needed
+    // Row reduction of Eq. text_scoring (visual keys: max over rows, registers: mean):
+    // over the lane's sub-blocks, then across the 32 lanes of a lane half (fixed
+    // order).  Rows past T_b hold exact zeros.
+    const bool regs = wactive && wkey0 < R;              // keys whose row sum is needed
     float mx[16], sm[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
@@ -501,22 +564,52 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int key = wkey0 + acc_key(r, hi);
-            if (key < S) scores[kb0 + key] = (mean_rows || key < R) ? sm[r] * invHT : mx[r] * invH;
+            if (key < S) scores[kb0 + key] = key < R ? sm[r] * invHT : mx[r] * invH;
         }
     }
 }
 
-template <int DS, bool HALF>
-static hipError_t stats_ds(const Prob& p, const void* q, const void* k, float* lse2, hipStream_t s) {
+template <int DS, bool HALF, bool COLSUM>
+static hipError_t stats_launch(const Prob& p, const void* q, const void* k, float* lse2,
+                               const float* lse_in, int lse_natural, float* part, hipStream_t s) {
     const size_t smem = text_stats_smem(DS * 16);
     static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&text_stats_kernel<DS, HALF>),
+        reinterpret_cast<const void*>(&text_stats_kernel<DS, HALF, COLSUM>),
         hipFuncAttributeMaxDynamicSharedMemorySize, (int)kScoreSmemMax);
     if (attr != hipSuccess) return attr;
     dim3 grid((p.max_rows + kTxtRows - 1) / kTxtRows, p.H, p.B);
-    hipLaunchKernelGGL((text_stats_kernel<DS, HALF>), grid, dim3(kStatsThreads), smem, s, p,
-                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse2);
+    hipLaunchKernelGGL((text_stats_kernel<DS, HALF, COLSUM>), grid, dim3(kStatsThreads), smem, s, p,
+                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse2,
+                       lse_in, lse_natural, part);
     return hipGetLastError();
+}
+
+template <int DS, bool HALF>
+static hipError_t stats_ds(const Prob& p, const void* q, const void* k, float* lse2, hipStream_t s) {
+    return stats_launch<DS, HALF, false>(p, q, k, lse2, nullptr, 0, nullptr, s);
+}
+
+template <int DS, bool HALF>
+static hipError_t colsum_ds(const Prob& p, const void* q, const void* k, const float* lse,
+                            int lse_natural, float* part, hipStream_t s) {
+    return stats_launch<DS, HALF, true>(p, q, k, nullptr, lse, lse_natural, part, s);
+}
+
+// Mutual scores: the mean over rows and heads of p, from the per-(row block, head)
+// column sums, added in a fixed order (row blocks outer, heads inner).
+__global__ __launch_bounds__(256) void text_colsum_reduce_kernel(Prob p, const float* __restrict__ part,
+                                                                 float* __restrict__ scores)
+{
+    const int b = blockIdx.y, s = blockIdx.x * 256 + threadIdx.x;
+    const int S = keys_of(p, b), T = rows_of(p, b);
+    if (s >= S) return;
+    const int nrb_max = (p.max_rows + kTxtRows - 1) / kTxtRows, nrb = (T + kTxtRows - 1) / kTxtRows;
+    const size_t smax = (size_t)(p.R + p.max_cands);
+    const float* pb = part + (size_t)b * nrb_max * p.H * smax + s;
+    float acc = 0.f;
+    for (int rb = 0; rb < nrb; ++rb)
+        for (int h = 0; h < p.H; ++h) acc += pb[((size_t)rb * p.H + h) * smax];
+    scores[k_begin(p, b) + s] = T > 0 ? acc * (1.f / ((float)p.H * (float)T)) : 0.f;
 }
 
 template <int DS, bool HALF, bool MULTI>
@@ -564,6 +657,20 @@ hipError_t launch_text_stats(const Prob& p, const void* q, const void* k, float*
 hipError_t launch_text_score(const Prob& p, const void* q, const void* k, const float* lse,
                              int lse_natural, float* scores, hipStream_t s) {
     OCCAM_D_SWITCH(score_ds, p, q, k, lse, lse_natural, scores, s)
+}
+
+static hipError_t colsum_any(const Prob& p, const void* q, const void* k, const float* lse,
+                             int lse_natural, float* part, hipStream_t s) {
+    OCCAM_D_SWITCH(colsum_ds, p, q, k, lse, lse_natural, part, s)
+}
+
+hipError_t launch_text_colsum(const Prob& p, const void* q, const void* k, const float* lse,
+                              int lse_natural, float* part, float* scores, hipStream_t s) {
+    const hipError_t e = colsum_any(p, q, k, lse, lse_natural, part, s);
+    if (e != hipSuccess) return e;
+    dim3 grid((p.R + p.max_cands + 255) / 256, p.B);
+    hipLaunchKernelGGL(text_colsum_reduce_kernel, grid, dim3(256), 0, s, p, part, scores);
+    return hipGetLastError();
 }
 
 }  // namespace occam

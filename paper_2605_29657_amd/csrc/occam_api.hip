@@ -20,7 +20,7 @@ struct Plan {
     int bf16;
     int text;          // 1: several anchor rows (MFMA path); 0: one anchor row (VALU path)
     int kpw;           // keys per workgroup of the one-row path
-    size_t off_logits, off_stats, off_lse2, off_scores, off_tau, off_slot, off_match, total;
+    size_t off_logits, off_stats, off_lse2, off_part, off_scores, off_tau, off_slot, off_match, total;
 };
 
 bool aligned(const void* ptr, size_t a) { return (reinterpret_cast<uintptr_t>(ptr) % a) == 0; }
@@ -68,6 +68,12 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
             return OCCAM_ERR_UNSUPPORTED;
         if (text_score_smem(H, ((d + 15) / 16) * 16) > kScoreSmemMax) return OCCAM_ERR_UNSUPPORTED;
         P.off_lse2 = off; off = align_up(off + (size_t)rows_cap * H * sizeof(float));
+        if (P.p.mean_rows) {
+            // Column sums of mutual scoring, per (sample, 128-row block, head, key).
+            P.off_part = off;
+            off = align_up(off + (size_t)B * ((max_rows + kTxtRows - 1) / kTxtRows) * H *
+                                     (R + (size_t)max_cands) * sizeof(float));
+        }
     } else {
         P.kpw = cls_keys_per_wg(H, x.num_kv_heads, d, bf16 ? 2 : 4);
         const int NC = d / (bf16 ? 8 : 4);
@@ -141,11 +147,18 @@ inline occam_status hip_ok(hipError_t e) { return e == hipSuccess ? OCCAM_OK : O
 occam_status run_score(const Plan& P, const void* q, const void* k, const float* row_lse,
                        float* scores, void* ws, hipStream_t s) {
     if (P.text) {
-        if (row_lse) return hip_ok(launch_text_score(P.p, q, k, row_lse, 1, scores, s));
-        float* lse2 = ws_at<float>(ws, P.off_lse2);
-        occam_status st = hip_ok(launch_text_stats(P.p, q, k, lse2, s));
-        if (st != OCCAM_OK) return st;
-        return hip_ok(launch_text_score(P.p, q, k, lse2, 0, scores, s));
+        const float* lse = row_lse;
+        if (!row_lse) {
+            float* lse2 = ws_at<float>(ws, P.off_lse2);
+            occam_status st = hip_ok(launch_text_stats(P.p, q, k, lse2, s));
+            if (st != OCCAM_OK) return st;
+            lse = lse2;
+        }
+        const int natural = row_lse ? 1 : 0;
+        if (P.p.mean_rows)
+            return hip_ok(launch_text_colsum(P.p, q, k, lse, natural, ws_at<float>(ws, P.off_part),
+                                             scores, s));
+        return hip_ok(launch_text_score(P.p, q, k, lse, natural, scores, s));
     }
     float* logits = ws_at<float>(ws, P.off_logits);
     float2* stats = ws_at<float2>(ws, P.off_stats);

@@ -200,6 +200,10 @@ hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const
                              const float* row_lse, float* scores, int kpw, hipStream_t s);
 hipError_t launch_text_stats(const Prob& p, const void* q, const void* k, float* lse2,
                              hipStream_t s);
+// Mutual scoring (every key: mean over rows): column sums per (row block, head) into
+// part [B][ceil(max_rows/128)][H][R + max_cands], then their fixed-order mean.
+hipError_t launch_text_colsum(const Prob& p, const void* q, const void* k, const float* lse,
+                              int lse_natural, float* part, float* scores, hipStream_t s);
 hipError_t launch_text_score(const Prob& p, const void* q, const void* k, const float* lse,
                              int lse_natural, float* scores, hipStream_t s);
 hipError_t launch_threshold(const Prob& p, const float* scores, float lambda, int reduce,
