@@ -261,6 +261,71 @@ def ablation_steps(torch, dv, dt, k1: float, k2: float, steps: int) -> dict:
                              "select_threshold_stage2_us": round(thr_us, 2)}}
 
 
+def chained_stage(txt, kept_idx, kept_offsets):
+    """Stage II over the tokens Stage I kept: per sample the R register rows and the
+    kept visual rows of the text-stage keys and payload, in Stage I's ascending order."""
+    from paper_2605_29657_amd import synth
+    B, R = txt.B, txt.R
+    n1 = np.diff(kept_offsets).astype(np.int64)
+    co = np.concatenate([[0], np.cumsum(txt.N)])
+    krows, vis_rows = [], []
+    for b in range(B):
+        kept = kept_idx[kept_offsets[b]:kept_offsets[b + 1]].astype(np.int64)
+        krows.append(txt.k_off[b] + np.arange(R))
+        krows.append(txt.k_off[b] + R + kept)
+        vis_rows.append((b, kept))
+    krows = np.concatenate(krows)
+    payload = []
+    for pl in txt.payload:
+        sel = []
+        for b, kept in vis_rows:
+            base = co[b] + b * pl.pad_rows
+            if pl.pad_rows:
+                sel.append(base + np.arange(pl.pad_rows))
+            sel.append(base + pl.row0 + kept)
+        payload.append(synth.Payload(pl.name, pl.rows[np.concatenate(sel)], pl.pad_rows, pl.row0))
+    return synth.StageBatch(workload=txt.workload, stage=txt.stage, dtype=txt.dtype, B=B, R=R,
+                            H=txt.H, Hkv=txt.Hkv, d=txt.d, T=txt.T, N=n1, q_off=txt.q_off,
+                            k_off=np.concatenate([[0], np.cumsum(R + n1)]).astype(np.int64),
+                            q=txt.q, k=txt.k[krows], payload=payload)
+
+
+def stage_breakdown(torch, dv, dt, txt, lam1: float, lam2: float, steps: int) -> dict:
+    """Each stage alone, and the chained pipeline: Stage II over the R + N1 tokens that
+    Stage I kept (its keys and payload rows staged untimed), index_map = Stage I's
+    indices, so that Stage II reports original token indices."""
+    from paper_2605_29657_amd.runner import DeviceStage
+
+    def timed(fn, n):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    B = dv.sb.B
+    ms1 = timed(lambda: dv.prune(lam1), steps)
+    ms2 = timed(lambda: dt.prune(lam2), steps)
+    kept_idx = dv.out["kept_idx"].cpu().numpy()
+    kept_off = dv.out["kept_offsets"].cpu().numpy()
+    ch = chained_stage(txt, kept_idx, kept_off)
+    dc = DeviceStage(ch, ragged=True)
+    imap = dv.out["kept_idx"][:int(kept_off[-1])].clone()
+    ms2c = timed(lambda: dc.prune(lam2, index_map=imap), steps)
+    kept2c = dc.out["kept_count"].float().mean().item()
+    del dc
+    return {"stage1_ms": round(ms1, 4), "stage2_ms": round(ms2, 4),
+            "chained": {"stage2_keys_mean": float(np.mean(ch.N + ch.R)),
+                        "stage2_ms": round(ms2c, 4), "step_ms": round(ms1 + ms2c, 4),
+                        "images_s": round(B / ((ms1 + ms2c) * 1e-3), 1),
+                        "kept_stage2_mean": kept2c}}
+
+
 def score_source_sha256() -> str:
     """sha256 of the sources the Stage II scoring kernel is built from."""
     import hashlib
@@ -463,6 +528,10 @@ def main():
     log("register redirect: %.1f us" % rec["register_redirect"]["us"])
     rec["budget_matching"] = budget_matching_bench(torch)
     log("budget matching: %.1f us" % rec["budget_matching"]["us"])
+    rec["stages"] = stage_breakdown(torch, dv, dt, txt, lam1, lam2, max(10, args.steps // 2))
+    log("stage I alone %.3f ms, stage II alone %.3f ms; chained step %.3f ms (%.0f keys)" % (
+        rec["stages"]["stage1_ms"], rec["stages"]["stage2_ms"], rec["stages"]["chained"]["step_ms"],
+        rec["stages"]["chained"]["stage2_keys_mean"]))
     rec["ablation"] = ablation_steps(torch, dv, dt, float(kept1.mean()), float(kept2.mean()),
                                      max(10, args.steps // 2))
     log("ablation: mean threshold %.3f ms/step, fixed budget %.3f ms/step" % (
