@@ -107,32 +107,43 @@ __device__ __forceinline__ void wait_vmem_le() {
 // fixed-order sum over the partials (text_colsum_reduce).  Both modes stream the keys
 // the same way; the column sums use the MFMA the other way round (rows as the A
 // operand), so that a lane holds 16 rows of one key and sums them in registers.
-template <int DS, bool HALF, bool COLSUM>
+template <int DS, bool HALF, bool COLSUM, int RG>
 __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     float* __restrict__ lse2, const float* __restrict__ lse_in, int lse_natural,
     float* __restrict__ part)
 {
-    // kStatsThreads / 64 waves: wave w owns rows [64*(w&1), +64) of the row block and
-    // the key stream ks = w>>1 (key blocks kbi = ks mod kStreams).  The two waves of a
-    // stream consume the same key blocks, so each block is copied once per pair,
-    // global -> LDS, into a ring of kStatsRing stages per stream: kStatsRing - 1 blocks
-    // are in flight while one is used.  A block is 32 keys x NCH 16-byte chunks; chunk c of key j sits in LDS
-    // unit j*NCH + (c ^ (j & SW)), SW = NCH - 1 when NCH is a power of two (else 0),
-    // so a copy writes whole 256-byte key slices and the MFMA fragment reads of 32
+    // kStatsThreads / 64 waves in kStreams key streams of RG waves each: wave w owns the
+    // RPW = 128 / RG rows [rg*RPW, +RPW) of the row block (rg = w % RG) and the key
+    // stream ks = w / RG (key blocks kbi = ks mod kStreams).  The RG waves of a stream
+    // consume the same key blocks, so each block is copied once per stream, global ->
+    // LDS, into a ring of kStatsRing stages per stream: kStatsRing - 1 blocks are in
+    // flight while one is used.  RG = 4 (32 rows per wave) needs half the registers of
+    // RG = 2 and runs more waves per SIMD; it is used when the rows span several blocks.
+    // A block is 32 keys x NCH 16-byte chunks; chunk c of key j sits in LDS unit
+    // j*NCH + (c ^ (j & SW)), SW = NCH - 1 when NCH is a power of two (else 0), so a
+    // copy writes whole 256-byte key slices and the MFMA fragment reads of 32
     // consecutive keys spread over the banks.
-    constexpr int kStreams = kStatsThreads / kWave / 2;
+    static_assert(RG == 2 || RG == 4, "row groups per stream");
+    constexpr int RPW = kTxtRows / RG;               // rows per wave
+    constexpr int NSBW = RPW / 32;                   // 32-row sub-blocks per wave
+    constexpr int kStreams = kStatsThreads / kWave / RG;
     constexpr int NCH = 2 * DS;                      // 16-byte chunks per key row
     constexpr int UNITS = 32 * NCH;                  // 16-byte units per block
     constexpr int COPIES = UNITS / kWave;            // = DS copies of 64 lanes per block
-    constexpr int MINE0 = (COPIES + 1) / 2, MINE1 = COPIES / 2;   // copies per pair member
+    constexpr int MINE = (COPIES + RG - 1) / RG;     // most copies a stream member issues
+    constexpr int MINE_MIN = COPIES / RG;            // fewest copies a stream member issues
     constexpr int SW = (NCH & (NCH - 1)) == 0 ? NCH - 1 : 0;
     extern __shared__ __attribute__((aligned(16))) char smem_raw[];
     u32x4* ring = reinterpret_cast<u32x4*>(smem_raw);              // [stream][stage][UNITS]
     float* red_m = reinterpret_cast<float*>(ring + kStreams * kStatsRing * UNITS);
     float* red_z = red_m + kStreams * kTxtRows;
 
-    const int tblk = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    // Task = (sample, head, row block), row blocks fastest, XCD-aware: the row blocks of
+    // one (sample, head) read the same keys and meet in one L2.
+    const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
+    const int task = xcd_remap((int)blockIdx.x, nrb * p.H * p.B);
+    const int tblk = task % nrb, h = (task / nrb) % p.H, b = task / (nrb * p.H);
     const int T = rows_of(p, b);
     const int t0 = tblk * kTxtRows;
     if (t0 >= T) return;
@@ -140,32 +151,32 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform
     const int hi = lane >> 5, lo = lane & 31;
-    const int rh = wave & 1, ks = wave >> 1;
+    const int rg = wave % RG, ks = wave / RG;
     const int H = p.H, Hkv = p.Hkv, d = p.d;
     const int g = h / (H / Hkv);
-    const int tw = t0 + rh * 64;                       // first row of this wave
-    const int nsb = max(0, min(2, (T - tw + 31) >> 5));
+    const int tw = t0 + rg * RPW;                      // first row of this wave
+    const int nsb = max(0, min(NSBW, (T - tw + 31) >> 5));
     const int qb = q_begin(p, b), kb0 = k_begin(p, b);
     const float c2 = p.scale * kLog2e;
 
-    bf16x8 qf[2][DS];
+    bf16x8 qf[NSBW][DS];
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
+    for (int sb = 0; sb < NSBW; ++sb) {
         const int t = min(tw + sb * 32 + lo, T - 1);
         const uint16_t* qrow = q + ((size_t)(qb + t) * H + h) * d;
 #pragma unroll
         for (int kk = 0; kk < DS; ++kk) qf[sb][kk] = as_bf16x8(frag16<DS, HALF>(qrow, kk, hi));
     }
 
-    float m[2], z[2];
+    float m[NSBW], z[NSBW];
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) { m[sb] = -INFINITY; z[sb] = 0.f; }
+    for (int sb = 0; sb < NSBW; ++sb) { m[sb] = -INFINITY; z[sb] = 0.f; }
     // COLSUM: base-2 normaliser of the 16 rows this lane holds in each sub-block (row
     // 8*(r/4) + 4*hi + r%4 of the sub-block); rows past T_b get +inf and weigh 0.
-    float lsev[COLSUM ? 2 : 1][16];
+    float lsev[COLSUM ? NSBW : 1][16];
     if (COLSUM) {
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb)
+        for (int sb = 0; sb < NSBW; ++sb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
                 const int t = tw + sb * 32 + acc_key(r, hi);
@@ -186,14 +197,14 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     const uint32_t sring_lds = lds_addr(sring);
 
     // Copy block j of this stream (clamped to the stream's last block) into its stage.
-    // Copy c of the block fills units 64c .. 64c+63; this wave issues c = rh, rh+2, ...
+    // Copy c of the block fills units 64c .. 64c+63; this wave issues c = rg, rg+RG, ...
     // Lane offsets inside a block are fixed (key kc = u / NCH of the block, chunk
     // (u % NCH) ^ (kc & SW)); only a block running past S_b clamps its keys.  The pad
     // chunk past d (HALF) reads chunk 0 of the key: its fragment is zeroed below.
-    uint32_t coff[MINE0];
+    uint32_t coff[MINE];
 #pragma unroll
-    for (int i = 0; i < MINE0; ++i) {
-        const int u = (rh + 2 * i) * kWave + lane;
+    for (int i = 0; i < MINE; ++i) {
+        const int u = min(rg + RG * i, COPIES - 1) * kWave + lane;
         const int kc = u / NCH, ch = (u % NCH) ^ (kc & SW);
         const int e = (HALF && ch == NCH - 1) ? 0 : ch * 8;
         coff[i] = (uint32_t)(kc * kstride + e) * 2u;
@@ -207,8 +218,8 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
         const uint32_t dst = sring_lds + (uint32_t)((jj % kStatsRing) * UNITS * 16);
         const bool full = kbi * 32 + 32 <= S;
 #pragma unroll
-        for (int i = 0; i < MINE0; ++i) {
-            const int c = rh + 2 * i;
+        for (int i = 0; i < MINE; ++i) {
+            const int c = rg + RG * i;
             if (c >= COPIES) break;
             uint32_t off = coff[i];
             if (!full) {
@@ -235,54 +246,63 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
             const u32x4 zero = {0u, 0u, 0u, 0u};
             kf[kk] = (HALF && kk == DS - 1 && hi) ? zero : v;
         }
-        f32x16 acc[2];
+        f32x16 acc[NSBW];
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb) acc[sb] = f32x16{};
+        for (int sb = 0; sb < NSBW; ++sb) acc[sb] = f32x16{};
         if (COLSUM) {
             // Rows as the A operand: lane (key lo, half hi) holds rows acc_key(r, hi).
+            // Both sub-blocks always: a branch between the MFMAs costs more than the
+            // clamped rows of a partial second sub-block (whose terms are skipped below).
 #pragma unroll
-            for (int kk = 0; kk < DS; ++kk) {
-                acc[0] = mfma32(qf[0][kk], as_bf16x8(kf[kk]), acc[0]);
-                if (nsb > 1) acc[1] = mfma32(qf[1][kk], as_bf16x8(kf[kk]), acc[1]);
-            }
-            float cs = 0.f;
+            for (int kk = 0; kk < DS; ++kk)
 #pragma unroll
-            for (int sb = 0; sb < 2; ++sb) {
+                for (int sb = 0; sb < NSBW; ++sb)
+                    acc[sb] = mfma32(qf[sb][kk], as_bf16x8(kf[kk]), acc[sb]);
+            // Four partial sums (r mod 4) keep the dependent add chains short.
+            float c4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int sb = 0; sb < NSBW; ++sb) {
                 if (sb >= nsb) break;
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    cs += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -lsev[sb][r]));
+                    c4[r & 3] += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -lsev[sb][r]));
             }
+            const float cs = (c4[0] + c4[1]) + (c4[2] + c4[3]);
             return cs + __shfl_xor(cs, 32);
         }
 #pragma unroll
-        for (int kk = 0; kk < DS; ++kk) {
-            acc[0] = mfma32(as_bf16x8(kf[kk]), qf[0][kk], acc[0]);
-            if (nsb > 1) acc[1] = mfma32(as_bf16x8(kf[kk]), qf[1][kk], acc[1]);
-        }
+        for (int kk = 0; kk < DS; ++kk)
 #pragma unroll
-        for (int sb = 0; sb < 2; ++sb) {
+            for (int sb = 0; sb < NSBW; ++sb)
+                acc[sb] = mfma32(as_bf16x8(kf[kk]), qf[sb][kk], acc[sb]);
+#pragma unroll
+        for (int sb = 0; sb < NSBW; ++sb) {
             if (sb >= nsb) break;
-            float mx = -INFINITY;
+            // Maximum and sum over the lane's 16 keys in four partial chains (r mod 4).
+            float m4[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
             if (nvalid >= 32) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, acc[sb][r]);
+                for (int r = 0; r < 16; ++r) m4[r & 3] = fmaxf(m4[r & 3], acc[sb][r]);
             } else {
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    if (acc_key(r, hi) < nvalid) mx = fmaxf(mx, acc[sb][r]);
+                    if (acc_key(r, hi) < nvalid) m4[r & 3] = fmaxf(m4[r & 3], acc[sb][r]);
             }
+            const float mx = fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3]));
             if (mx == -INFINITY) continue;
             const float mn = fmaxf(m[sb], mx * c2);
-            float sum = 0.f;
+            float s4[4] = {0.f, 0.f, 0.f, 0.f};
             if (nvalid >= 32) {
 #pragma unroll
-                for (int r = 0; r < 16; ++r) sum += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -mn));
+                for (int r = 0; r < 16; ++r)
+                    s4[r & 3] += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -mn));
             } else {
 #pragma unroll
                 for (int r = 0; r < 16; ++r)
-                    if (acc_key(r, hi) < nvalid) sum += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -mn));
+                    if (acc_key(r, hi) < nvalid)
+                        s4[r & 3] += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -mn));
             }
+            const float sum = (s4[0] + s4[1]) + (s4[2] + s4[3]);
             z[sb] = z[sb] * __builtin_amdgcn_exp2f(m[sb] - mn) + sum;
             m[sb] = mn;
         }
@@ -292,48 +312,52 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     // Every wave runs the same number of iterations (the most any stream has), so the
     // barriers match; a stream past its last block only re-issues its last block.
     const int iters = (nkb + kStreams - 1) / kStreams;
-    // COLSUM: the two row halves of a stream leave their column sums of block j in
-    // sums[j & 1][ks][rh][key]; after the next barrier the rh = 0 wave adds the pair (in
-    // that order) and stores the workgroup's partial.
+    // COLSUM: the RG waves of a stream leave their column sums of block j in
+    // sums[j & 1][ks][rg][key] (red_m and red_z together); after the next barrier the
+    // rg = 0 wave adds them in order of rg and stores the workgroup's partial.
     float* sums = red_m;
-    float* prow = part + (((size_t)b * ((p.max_rows + kTxtRows - 1) / kTxtRows) + tblk) * H + h) *
-                             (size_t)(p.R + p.max_cands);
+    float* prow = part + (((size_t)b * nrb + tblk) * H + h) * (size_t)(p.R + p.max_cands);
     auto store_sums = [&](int j) {
-        const float* sp = sums + ((j & 1) * kStreams + ks) * 64;
+        const float* sp = sums + ((j & 1) * kStreams + ks) * (RG * 32);
         const int key = (ks + j * kStreams) * 32 + lane;
-        if (lane < 32 && key < S) prow[key] = sp[lane] + sp[32 + lane];
+        if (lane < 32 && key < S) {
+            float v = sp[lane];
+#pragma unroll
+            for (int w = 1; w < RG; ++w) v += sp[w * 32 + lane];
+            prow[key] = v;
+        }
     };
 #pragma unroll
     for (int j = 0; j < kStatsRing - 1; ++j) issue(j);
     for (int i = 0; i < iters; ++i) {
-        // Own copies of block i have landed once at most kStatsRing-2 later blocks remain.
-        if (rh == 0) wait_vmem_le<(kStatsRing - 2) * MINE0>();
-        else wait_vmem_le<(kStatsRing - 2) * MINE1>();
+        // Own copies of block i have landed once at most kStatsRing-2 later blocks remain
+        // (counted with the fewest copies a member issues: a stronger wait for the others).
+        wait_vmem_le<(kStatsRing - 2) * MINE_MIN>();
         __syncthreads();                 // partner's copies landed; stage (i-1) is free
         issue(i + kStatsRing - 1);
-        if (COLSUM && rh == 0 && i >= 1 && i - 1 < nmine) store_sums(i - 1);
+        if (COLSUM && rg == 0 && i >= 1 && i - 1 < nmine) store_sums(i - 1);
         if (i < nmine) {
             float cs = 0.f;
             if (nsb > 0) cs = block(ks + i * kStreams, sring + (i % kStatsRing) * UNITS);
-            if (COLSUM && hi == 0) sums[((i & 1) * kStreams + ks) * 64 + rh * 32 + lo] = cs;
+            if (COLSUM && hi == 0) sums[((i & 1) * kStreams + ks) * (RG * 32) + rg * 32 + lo] = cs;
         }
     }
     wait_vmem_le<0>();
     if (COLSUM) {
         __syncthreads();
-        if (rh == 0 && iters >= 1 && iters - 1 < nmine) store_sums(iters - 1);
+        if (rg == 0 && iters >= 1 && iters - 1 < nmine) store_sums(iters - 1);
         return;
     }
 
     // Merge the two lane halves (same rows, different keys), then the key streams.
 #pragma unroll
-    for (int sb = 0; sb < 2; ++sb) {
+    for (int sb = 0; sb < NSBW; ++sb) {
         const float mo = __shfl_xor(m[sb], 32);
         const float zo = __shfl_xor(z[sb], 32);
         merge_pair(m[sb], z[sb], mo, zo);
         if (hi == 0) {
-            red_m[ks * kTxtRows + rh * 64 + sb * 32 + lo] = m[sb];
-            red_z[ks * kTxtRows + rh * 64 + sb * 32 + lo] = z[sb];
+            red_m[ks * kTxtRows + rg * RPW + sb * 32 + lo] = m[sb];
+            red_z[ks * kTxtRows + rg * RPW + sb * 32 + lo] = z[sb];
         }
     }
     __syncthreads();
@@ -569,19 +593,29 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     }
 }
 
+template <int DS, bool HALF, bool COLSUM, int RG>
+static hipError_t stats_launch_rg(const Prob& p, const void* q, const void* k, float* lse2,
+                                  const float* lse_in, int lse_natural, float* part, hipStream_t s) {
+    const size_t smem = text_stats_smem(DS * 16, RG);
+    static const hipError_t attr = hipFuncSetAttribute(
+        reinterpret_cast<const void*>(&text_stats_kernel<DS, HALF, COLSUM, RG>),
+        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kScoreSmemMax);
+    if (attr != hipSuccess) return attr;
+    dim3 grid((p.max_rows + kTxtRows - 1) / kTxtRows * p.H * p.B);
+    hipLaunchKernelGGL((text_stats_kernel<DS, HALF, COLSUM, RG>), grid, dim3(kStatsThreads), smem,
+                       s, p, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse2,
+                       lse_in, lse_natural, part);
+    return hipGetLastError();
+}
+
+// Rows spanning several 128-row blocks (long anchor sets, mutual scoring): four waves
+// of 32 rows per key stream; one block: two waves of 64 rows per stream.
 template <int DS, bool HALF, bool COLSUM>
 static hipError_t stats_launch(const Prob& p, const void* q, const void* k, float* lse2,
                                const float* lse_in, int lse_natural, float* part, hipStream_t s) {
-    const size_t smem = text_stats_smem(DS * 16);
-    static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&text_stats_kernel<DS, HALF, COLSUM>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kScoreSmemMax);
-    if (attr != hipSuccess) return attr;
-    dim3 grid((p.max_rows + kTxtRows - 1) / kTxtRows, p.H, p.B);
-    hipLaunchKernelGGL((text_stats_kernel<DS, HALF, COLSUM>), grid, dim3(kStatsThreads), smem, s, p,
-                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse2,
-                       lse_in, lse_natural, part);
-    return hipGetLastError();
+    if (p.max_rows > kTxtRows)
+        return stats_launch_rg<DS, HALF, COLSUM, 4>(p, q, k, lse2, lse_in, lse_natural, part, s);
+    return stats_launch_rg<DS, HALF, COLSUM, 2>(p, q, k, lse2, lse_in, lse_natural, part, s);
 }
 
 template <int DS, bool HALF>

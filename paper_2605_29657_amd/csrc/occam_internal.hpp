@@ -155,9 +155,10 @@ inline size_t text_score_smem(int H, int d16) {
 // the head slices faster than deeper rings at fewer workgroups per CU: the scattered
 // 256-byte slices stream better with fewer requests outstanding per CU.
 constexpr int kStatsRing = 2;
-inline size_t text_stats_smem(int d16) {
-    return (size_t)(kStatsThreads / kWave / 2) * kStatsRing * 32 * d16 * 2 +
-           2 * (size_t)(kStatsThreads / kWave / 2) * kTxtRows * 4;
+// rg: waves per key stream (2 or 4).
+inline size_t text_stats_smem(int d16, int rg) {
+    return (size_t)(kStatsThreads / kWave / rg) * kStatsRing * 32 * d16 * 2 +
+           2 * (size_t)(kStatsThreads / kWave / rg) * kTxtRows * 4;
 }
 
 // Anchor-path keys per workgroup for a given row geometry.
