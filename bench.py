@@ -326,6 +326,53 @@ def stage_breakdown(torch, dv, dt, txt, lam1: float, lam2: float, steps: int) ->
                         "kept_stage2_mean": kept2c}}
 
 
+def workload_step(torch, name: str, steps: int) -> dict:
+    """The headline step (Stage I prune + Stage II prune over all tokens) on another
+    workload shape: images/s, the step's algorithmic bytes over its time, and the text
+    stage's algorithmic MFMA rate (one Q K^T)."""
+    from paper_2605_29657_amd import synth
+    from paper_2605_29657_amd.runner import DeviceStage
+    with open(os.path.join(ROOT, "tests", "golden", "lambdas.json")) as f:
+        lams = json.load(f)[name]
+    lam1 = float(np.float32(lams["vis"]["lam"]))
+    lam2 = float(np.float32(lams["txt"]["lam"]))
+    vis = synth.make_stage(name, "vis")
+    txt = synth.make_stage(name, "txt")
+    dv = DeviceStage(vis, ragged=vis.ragged)
+    dt = DeviceStage(txt, ragged=txt.ragged)
+
+    def step():
+        dv.prune(lam1)
+        dt.prune(lam2)
+
+    for _ in range(2):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        step()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    kept1 = dv.out["kept_count"].cpu().numpy()
+    kept2 = dt.out["kept_count"].cpu().numpy()
+    nbytes = stage_bytes(vis, kept1)["total"] + stage_bytes(txt, kept2)["total"]
+    flops = float(np.sum(2.0 * txt.T.astype(np.float64) * (txt.N + txt.R) * txt.H * txt.d))
+    out = {"workload": "%s: B=%d, N in [%d, %d], R=%d; Stage I H=%d d=%d %s; Stage II T in [%d, %d] "
+                       "H=%d d=%d" % (name, vis.B, int(vis.N.min()), int(vis.N.max()), vis.R, vis.H,
+                                      vis.d, vis.dtype, int(txt.T.min()), int(txt.T.max()), txt.H,
+                                      txt.d),
+           "ms_per_step": round(ms, 4), "images_s": round(vis.B / (ms * 1e-3), 1),
+           "achieved_hbm_gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+           "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+           "text_mfma_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+           "kept_stage1_mean": float(np.mean(kept1)), "kept_stage2_mean": float(np.mean(kept2))}
+    del dv, dt
+    torch.cuda.empty_cache()
+    return out
+
+
 def score_source_sha256() -> str:
     """sha256 of the sources the Stage II scoring kernel is built from."""
     import hashlib
@@ -365,6 +412,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-mutual", action="store_true",
                     help="skip the secondary mutual-scoring Stage I measurement")
+    ap.add_argument("--no-workloads", action="store_true",
+                    help="skip the LLaVA-1.5, Qwen3-VL and video steps")
     ap.add_argument("--mutual-only", action="store_true",
                     help="run and print only the mutual-scoring Stage I measurement")
     ap.add_argument("--kernel-reps", type=int, default=20,
@@ -537,8 +586,17 @@ def main():
     log("ablation: mean threshold %.3f ms/step, fixed budget %.3f ms/step" % (
         rec["ablation"]["mean_threshold"]["ms_per_step"],
         rec["ablation"]["fixed_budget"]["ms_per_step"]))
-    if not args.no_mutual:
+    if not args.no_workloads:
         del dv, dt
+        torch.cuda.empty_cache()
+        rec["workloads"] = {}
+        for wname in ("llava15", "qwen3vl_ragged", "video"):
+            rec["workloads"][wname] = workload_step(torch, wname, 10)
+            log("%s: %.3f ms/step, %.0f images/s, %.1f%% of HBM peak" % (
+                wname, rec["workloads"][wname]["ms_per_step"], rec["workloads"][wname]["images_s"],
+                100 * rec["workloads"][wname]["hbm_frac"]))
+    if not args.no_mutual:
+        dv = dt = None
         torch.cuda.empty_cache()
         rec["mutual_stage1"] = mutual_stage1(torch, max(5, args.steps // 5), 2,
                                              not args.no_cpu_baseline)

@@ -153,10 +153,11 @@ __device__ __forceinline__ float lane_group_sum(float x) {
     return x;
 }
 
-// Streaming form of cls_logits for H == Hkv with NC (a power of two <= 16) 16-byte
-// chunks per head and NJ = H * NC / 64 wave loads per key row.  Lane l owns chunks
-// ci = l + 64 j of every key row (head ci / NC, part ci % NC) and keeps the matching
-// query elements in registers.  Each wave walks its keys KB at a time (KB rows of
+// Streaming form of cls_logits for H == Hkv with nc <= 16 16-byte chunks per head,
+// NC = nc rounded up to a power of two lanes per head and NJ = H * NC / 64 wave loads
+// per key row.  Lane l owns the lane slots ci = l + 64 j of every key row (head
+// ci / NC, chunk ci % NC; a slot past the head's nc chunks rereads its last chunk
+// against a zero query) and keeps the matching query elements in registers.  Each wave walks its keys KB at a time (KB rows of
 // coalesced 1 KB loads in flight), reduces the per-chunk partial dot products over
 // the NC lanes of a head with DPP, writes the scaled logit and folds it into a
 // per-head online (max, sum exp) pair held by those lanes.  The four waves' pairs are
@@ -164,7 +165,7 @@ __device__ __forceinline__ float lane_group_sum(float x) {
 template <bool BF16, int NC, int NJ>
 __global__ __launch_bounds__(kClsThreads) void cls_stream_kernel(
     Prob p, const void* __restrict__ qv, const void* __restrict__ kv,
-    float* __restrict__ logits, float2* __restrict__ stats, int kpw, int nchunks)
+    float* __restrict__ logits, float2* __restrict__ stats, int kpw, int nchunks, int nc)
 {
     constexpr int CE = BF16 ? 8 : 4;                 // elements per 16-byte chunk
     constexpr int KB = 4;                            // key rows in flight per wave
@@ -179,14 +180,21 @@ __global__ __launch_bounds__(kClsThreads) void cls_stream_kernel(
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const float scale = p.scale;
 
-    // Query elements of this lane's chunks, as float.
+    // Query elements of this lane's chunks, as float (zero for slots past nc), and the
+    // chunk each slot loads within a key row.
     float qf[NJ][CE];
+    int koff[NJ];
     const int qrow = q_begin(p, b);
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
         const int ci = lane + 64 * j;
-        const int h = ci / NC, e0 = (ci % NC) * CE;
-        if (BF16) {
+        const int h = ci / NC, part = ci % NC;
+        const int e0 = min(part, nc - 1) * CE;
+        koff[j] = h * nc + min(part, nc - 1);
+        if (part >= nc) {
+#pragma unroll
+            for (int e = 0; e < CE; ++e) qf[j][e] = 0.f;
+        } else if (BF16) {
             const uint16_t* q16 = static_cast<const uint16_t*>(qv) + ((size_t)qrow * H + h) * d + e0;
 #pragma unroll
             for (int e = 0; e < CE; ++e) qf[j][e] = __uint_as_float(static_cast<uint32_t>(q16[e]) << 16);
@@ -200,7 +208,8 @@ __global__ __launch_bounds__(kClsThreads) void cls_stream_kernel(
     float m[NJ], z[NJ];
 #pragma unroll
     for (int j = 0; j < NJ; ++j) { m[j] = -INFINITY; z[j] = 0.f; }
-    const u32x4* kbase = static_cast<const u32x4*>(kv) + ((size_t)k_begin(p, b) + s0) * (NJ * 64);
+    const int rowc = H * nc;                         // 16-byte chunks per key row
+    const u32x4* kbase = static_cast<const u32x4*>(kv) + ((size_t)k_begin(p, b) + s0) * rowc;
     float* lout = logits + ((size_t)k_begin(p, b) + s0) * H;
 
     for (int k0 = wave * KB; k0 < nk; k0 += NW * KB) {
@@ -210,7 +219,7 @@ __global__ __launch_bounds__(kClsThreads) void cls_stream_kernel(
             const int key = min(k0 + i, nk - 1);     // clamped rows are loaded, not used
 #pragma unroll
             for (int j = 0; j < NJ; ++j)
-                w[i][j] = __builtin_nontemporal_load(kbase + (size_t)key * (NJ * 64) + lane + 64 * j);
+                w[i][j] = __builtin_nontemporal_load(kbase + (size_t)key * rowc + koff[j]);
         }
 #pragma unroll
         for (int i = 0; i < KB; ++i) {
@@ -337,13 +346,14 @@ static size_t cls_logits_smem(const Prob& p, int bf16, int kpw) {
 template <bool BF16, int NC>
 static hipError_t cls_stream_launch(const Prob& p, const void* q, const void* k, float* logits,
                                     float2* stats, int kpw, hipStream_t s) {
+    const int nc = p.d * (BF16 ? 2 : 4) / 16;
     const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
     dim3 grid(nchunks, p.B);
     switch (NC * p.Hkv / 64) {
-    case 1: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 1>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks); break;
-    case 2: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 2>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks); break;
-    case 3: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 3>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks); break;
-    case 4: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 4>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks); break;
+    case 1: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 1>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks, nc); break;
+    case 2: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 2>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks, nc); break;
+    case 3: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 3>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks, nc); break;
+    case 4: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 4>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks, nc); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

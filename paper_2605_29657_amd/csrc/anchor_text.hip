@@ -370,13 +370,14 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     }
 }
 
-template <int DS, bool HALF, bool MULTI>
+template <int DS, bool HALF>
 __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
-    const float* __restrict__ lse, int lse_natural, float* __restrict__ scores)
+    const float* __restrict__ lse, int lse_natural, float* __restrict__ scores,
+    float* __restrict__ part)
 {
-    // 4 waves: wave w owns the 32 keys [s_lo + 32 w, +32) and all 128 rows of the
-    // current row block (4 sub-blocks of 32 rows, computed as two interleaved MFMA
+    // 4 waves: wave w owns the 32 keys [s_lo + 32 w, +32) and the 128 rows of the
+    // workgroup's row block (4 sub-blocks of 32 rows, computed as two interleaved MFMA
     // accumulator chains).  Two workgroups share a CU, so one workgroup's MFMAs
     // overlap the other's exponentials.
     //
@@ -396,16 +397,21 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     u32x4* qt = reinterpret_cast<u32x4*>(smem_raw);                         // [2][QTILE]
     float* l2t = reinterpret_cast<float*>(smem_raw + 2 * QTILE * 16);       // [H][128]
 
-    // Task = (sample, key chunk), XCD-aware: the chunks of one sample run on one XCD
-    // and share its L2 for the query tiles.  Samples in reverse order: the statistics
-    // pass streamed sample B-1 last, so its keys are the likeliest to still sit in the
-    // memory-side cache.
+    // Task = (sample, key chunk, row block), row blocks fastest, XCD-aware: the chunks
+    // of one sample run on one XCD and share its L2 for the query tiles, and the row
+    // blocks of one chunk read the same keys there.  Samples in reverse order: the
+    // statistics pass streamed sample B-1 last, so its keys are the likeliest to still
+    // sit in the memory-side cache.  With several row blocks (part != null) each writes
+    // its row maximum (visual keys) or row sum (registers) to part[b][row block][key]
+    // and text_rows_combine forms the scores.
     const int nchunk = (p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg;
-    const int task = xcd_remap((int)blockIdx.x, nchunk * p.B);
-    const int c = task % nchunk, b = p.B - 1 - task / nchunk;
+    const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
+    const int task = xcd_remap((int)blockIdx.x, nchunk * nrb * p.B);
+    const int rb = task % nrb, c = (task / nrb) % nchunk, b = p.B - 1 - task / (nrb * nchunk);
     const int S = keys_of(p, b);
     const int s_lo = c * kTxtKeysPerWg;
-    if (s_lo >= S) return;
+    const int t0 = rb * kTxtRows;
+    if (s_lo >= S || t0 >= rows_of(p, b)) return;
     const int T = rows_of(p, b);
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int hi = lane >> 5, lo = lane & 31;
@@ -474,16 +480,9 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
         }
     };
 
-    float vmax[MULTI ? 16 : 1], rsum[MULTI ? 16 : 1];
-    if (MULTI) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) { vmax[r] = 0.f; rsum[r] = 0.f; }
-    }
     float abar[4][16];
-
-    for (int t0 = 0; t0 < T; t0 += kTxtRows) {
+    {
         const int nsb = min(4, (T - t0 + 31) >> 5);
-        __syncthreads();  // previous row block is done with qt / l2t
         for (int i = tid; i < H * kTxtRows; i += kScoreThreads) {
             const int hh = i / kTxtRows, t = t0 + (i % kTxtRows);
             float v = INFINITY;
@@ -552,14 +551,6 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
             if (h + 1 >= H) break;
             head(h + 1, k1, k0);
         }
-        if (MULTI) {
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-                vmax[r] = fmaxf(vmax[r], fmaxf(fmaxf(abar[0][r], abar[1][r]),
-                                               fmaxf(abar[2][r], abar[3][r])));
-                rsum[r] += (abar[0][r] + abar[1][r]) + (abar[2][r] + abar[3][r]);
-            }
-        }
     }
 
     // Row reduction of Eq. text_scoring (visual keys: max over rows, registers: mean):
@@ -569,13 +560,8 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     float mx[16], sm[16];
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-        if (MULTI) {
-            mx[r] = vmax[r];
-            sm[r] = rsum[r];
-        } else {
-            mx[r] = fmaxf(fmaxf(abar[0][r], abar[1][r]), fmaxf(abar[2][r], abar[3][r]));
-            sm[r] = (abar[0][r] + abar[1][r]) + (abar[2][r] + abar[3][r]);
-        }
+        mx[r] = fmaxf(fmaxf(abar[0][r], abar[1][r]), fmaxf(abar[2][r], abar[3][r]));
+        sm[r] = (abar[0][r] + abar[1][r]) + (abar[2][r] + abar[3][r]);
 #pragma unroll
         for (int off = 16; off >= 1; off >>= 1) {
             mx[r] = fmaxf(mx[r], __shfl_xor(mx[r], off));
@@ -585,12 +571,37 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     if (wactive && lo == 0) {
         const float invH = 1.f / (float)H;
         const float invHT = 1.f / ((float)H * (float)T);
+        float* prow = part ? part + ((size_t)b * nrb + rb) * (size_t)(p.R + p.max_cands) : nullptr;
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
             const int key = wkey0 + acc_key(r, hi);
-            if (key < S) scores[kb0 + key] = key < R ? sm[r] * invHT : mx[r] * invH;
+            if (key >= S) continue;
+            if (prow) prow[key] = key < R ? sm[r] : mx[r];
+            else scores[kb0 + key] = key < R ? sm[r] * invHT : mx[r] * invH;
         }
     }
+}
+
+// Scores from the row blocks' partials: the maximum over row blocks (visual keys) or
+// the sum in row-block order (registers), then the head mean (and row mean).
+__global__ __launch_bounds__(256) void text_rows_combine_kernel(Prob p, const float* __restrict__ part,
+                                                                float* __restrict__ scores)
+{
+    const int b = blockIdx.y, s = blockIdx.x * 256 + threadIdx.x;
+    const int S = keys_of(p, b), T = rows_of(p, b);
+    if (s >= S) return;
+    const int nrb_max = (p.max_rows + kTxtRows - 1) / kTxtRows, nrb = (T + kTxtRows - 1) / kTxtRows;
+    const size_t smax = (size_t)(p.R + p.max_cands);
+    const float* pb = part + (size_t)b * nrb_max * smax + s;
+    float v = 0.f;
+    if (s < p.R) {
+        for (int rb = 0; rb < nrb; ++rb) v += pb[(size_t)rb * smax];
+        v *= 1.f / ((float)p.H * (float)T);
+    } else {
+        for (int rb = 0; rb < nrb; ++rb) v = fmaxf(v, pb[(size_t)rb * smax]);
+        v *= 1.f / (float)p.H;
+    }
+    scores[k_begin(p, b) + s] = v;
 }
 
 template <int DS, bool HALF, bool COLSUM, int RG>
@@ -646,27 +657,24 @@ __global__ __launch_bounds__(256) void text_colsum_reduce_kernel(Prob p, const f
     scores[k_begin(p, b) + s] = T > 0 ? acc * (1.f / ((float)p.H * (float)T)) : 0.f;
 }
 
-template <int DS, bool HALF, bool MULTI>
-static hipError_t score_launch(const Prob& p, const void* q, const void* k, const float* lse,
-                               int lse_natural, float* scores, hipStream_t s) {
+template <int DS, bool HALF>
+static hipError_t score_ds(const Prob& p, const void* q, const void* k, const float* lse,
+                           int lse_natural, float* scores, float* part, hipStream_t s) {
     const size_t smem = text_score_smem(p.H, DS * 16);
     // The tile needs more than the default 64 KB of dynamic LDS: raise the limit once.
     static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&text_score_kernel<DS, HALF, MULTI>),
+        reinterpret_cast<const void*>(&text_score_kernel<DS, HALF>),
         hipFuncAttributeMaxDynamicSharedMemorySize, (int)kScoreSmemMax);
     if (attr != hipSuccess) return attr;
-    dim3 grid((p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg * p.B);
-    hipLaunchKernelGGL((text_score_kernel<DS, HALF, MULTI>), grid, dim3(kScoreThreads), smem, s, p,
+    const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
+    dim3 grid((p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg * nrb * p.B);
+    hipLaunchKernelGGL((text_score_kernel<DS, HALF>), grid, dim3(kScoreThreads), smem, s, p,
                        static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
-                       lse_natural, scores);
+                       lse_natural, scores, nrb > 1 ? part : nullptr);
+    if (nrb == 1) return hipGetLastError();
+    dim3 cgrid((p.R + p.max_cands + 255) / 256, p.B);
+    hipLaunchKernelGGL(text_rows_combine_kernel, cgrid, dim3(256), 0, s, p, part, scores);
     return hipGetLastError();
-}
-
-template <int DS, bool HALF>
-static hipError_t score_ds(const Prob& p, const void* q, const void* k, const float* lse,
-                           int lse_natural, float* scores, hipStream_t s) {
-    if (p.max_rows > kTxtRows) return score_launch<DS, HALF, true>(p, q, k, lse, lse_natural, scores, s);
-    return score_launch<DS, HALF, false>(p, q, k, lse, lse_natural, scores, s);
 }
 
 // d = 16*DS (HALF = false) or 16*DS - 8 (HALF = true), d <= 128.
@@ -689,8 +697,8 @@ hipError_t launch_text_stats(const Prob& p, const void* q, const void* k, float*
 }
 
 hipError_t launch_text_score(const Prob& p, const void* q, const void* k, const float* lse,
-                             int lse_natural, float* scores, hipStream_t s) {
-    OCCAM_D_SWITCH(score_ds, p, q, k, lse, lse_natural, scores, s)
+                             int lse_natural, float* scores, float* part, hipStream_t s) {
+    OCCAM_D_SWITCH(score_ds, p, q, k, lse, lse_natural, scores, part, s)
 }
 
 static hipError_t colsum_any(const Prob& p, const void* q, const void* k, const float* lse,

@@ -68,11 +68,14 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
             return OCCAM_ERR_UNSUPPORTED;
         if (text_score_smem(H, ((d + 15) / 16) * 16) > kScoreSmemMax) return OCCAM_ERR_UNSUPPORTED;
         P.off_lse2 = off; off = align_up(off + (size_t)rows_cap * H * sizeof(float));
+        const size_t nrb = (max_rows + kTxtRows - 1) / kTxtRows;
+        P.off_part = off;
         if (P.p.mean_rows) {
             // Column sums of mutual scoring, per (sample, 128-row block, head, key).
-            P.off_part = off;
-            off = align_up(off + (size_t)B * ((max_rows + kTxtRows - 1) / kTxtRows) * H *
-                                     (R + (size_t)max_cands) * sizeof(float));
+            off = align_up(off + (size_t)B * nrb * H * (R + (size_t)max_cands) * sizeof(float));
+        } else if (nrb > 1) {
+            // Row maxima / sums of the max form, per (sample, 128-row block, key).
+            off = align_up(off + (size_t)B * nrb * (R + (size_t)max_cands) * sizeof(float));
         }
     } else {
         P.kpw = cls_keys_per_wg(H, x.num_kv_heads, d, bf16 ? 2 : 4);
@@ -155,10 +158,9 @@ occam_status run_score(const Plan& P, const void* q, const void* k, const float*
             lse = lse2;
         }
         const int natural = row_lse ? 1 : 0;
-        if (P.p.mean_rows)
-            return hip_ok(launch_text_colsum(P.p, q, k, lse, natural, ws_at<float>(ws, P.off_part),
-                                             scores, s));
-        return hip_ok(launch_text_score(P.p, q, k, lse, natural, scores, s));
+        float* part = ws_at<float>(ws, P.off_part);
+        if (P.p.mean_rows) return hip_ok(launch_text_colsum(P.p, q, k, lse, natural, part, scores, s));
+        return hip_ok(launch_text_score(P.p, q, k, lse, natural, scores, part, s));
     }
     float* logits = ws_at<float>(ws, P.off_logits);
     float2* stats = ws_at<float2>(ws, P.off_stats);

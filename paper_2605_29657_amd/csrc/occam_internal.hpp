@@ -165,13 +165,18 @@ inline size_t text_stats_smem(int d16, int rg) {
 // Streaming form of the one-row logits (cls_stream_kernel): every query head has its
 // own key head, a head is NC 16-byte chunks with NC a power of two up to 16, and a key
 // row is 1 to 4 whole 64-lane loads.  Returns NC when the form applies, else 0.
+// Lanes per head of the streaming one-row form: the head's 16-byte chunk count rounded
+// up to a power of two (at most 16; lanes past the real chunks contribute zero), or 0
+// when the form does not apply.
 inline int cls_stream_nc(int H, int Hkv, int d, int elem_bytes) {
     if (H != Hkv || (d * elem_bytes) % 16 != 0) return 0;
     const int nc = d * elem_bytes / 16;
-    if (nc != 1 && nc != 2 && nc != 4 && nc != 8 && nc != 16) return 0;
-    const int cpk = nc * Hkv;
+    if (nc < 1 || nc > 16) return 0;
+    int ncp = 1;
+    while (ncp < nc) ncp *= 2;
+    const int cpk = ncp * Hkv;
     if (cpk % 64 != 0 || cpk / 64 > 4) return 0;
-    return nc;
+    return ncp;
 }
 constexpr int kClsStreamKeys = 128;    // keys per workgroup of the streaming form
 
@@ -205,8 +210,10 @@ hipError_t launch_text_stats(const Prob& p, const void* q, const void* k, float*
 // part [B][ceil(max_rows/128)][H][R + max_cands], then their fixed-order mean.
 hipError_t launch_text_colsum(const Prob& p, const void* q, const void* k, const float* lse,
                               int lse_natural, float* part, float* scores, hipStream_t s);
+// Max-over-rows scoring; with several 128-row blocks, per-block partials go to part
+// [B][ceil(max_rows/128)][R + max_cands] and a combine kernel forms the scores.
 hipError_t launch_text_score(const Prob& p, const void* q, const void* k, const float* lse,
-                             int lse_natural, float* scores, hipStream_t s);
+                             int lse_natural, float* scores, float* part, hipStream_t s);
 hipError_t launch_threshold(const Prob& p, const float* scores, float lambda, int reduce,
                             float* tau, hipStream_t s);
 hipError_t launch_select(const Prob& p, const float* scores, const float* tau, int fuse_tau,
