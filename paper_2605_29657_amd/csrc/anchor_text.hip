@@ -6,34 +6,42 @@
 // operand is a block of 32 keys and its B operand a block of 32 text rows, so
 // each lane of the accumulator holds 16 keys of ONE text row: reductions over
 // keys (the softmax statistics) stay inside a lane, and the head sum is an
-// element-wise accumulation in registers.
+// element-wise accumulation in registers.  (The column-sum form below swaps the
+// operands, so that a lane holds 16 rows of one key.)
 //
 // Every (row, head) softmax needs its normaliser before the head mean can be
 // formed, so the path has two passes over the keys:
 //
-// text_stats  grid (row block of 128, head, sample).  Each wave owns every
-//             4th block of 32 keys, keeps the 128 query rows of the head as
-//             MFMA B fragments in registers, and maintains an online
-//             (max, sum 2^x) pair per row; pairs are merged across the two
-//             lane halves and the 4 key streams in a fixed order.  Key blocks
-//             reach LDS through direct global -> LDS copies (a 4-stage ring
-//             per stream).  Writes the base-2 log-sum-exp lse2[row, head] of
-//             x = logit * log2(e).
-// text_score  one workgroup per (sample, block of 128 keys).  Each wave owns 32
-//             keys.  For every head the 128 x d query tile is copied global ->
-//             LDS (double-buffered) and the wave's key fragments are loaded into
-//             registers one head ahead, while p = 2^(x - lse2) of the current
-//             head is accumulated over heads per (key, row).  Afterwards the row
-//             reduction of Eq. text_scoring is applied: max over rows for visual
-//             keys, mean for registers, both over the head mean (1/H).  Rows
-//             beyond T_b carry lse2 = +inf and so contribute exactly 0.
+// text_stats  task (sample, head, row block of 128), XCD-aware.  Key streams of
+//             two waves x 64 rows (one row block) or four waves x 32 rows (rows
+//             spanning several blocks); each stream owns every kStreams-th block
+//             of 32 keys, the query rows of the head sit in registers as MFMA B
+//             fragments, and an online (max, sum 2^x) pair is kept per row;
+//             pairs are merged across the two lane halves and the streams in a
+//             fixed order.  Key blocks reach LDS through direct global -> LDS
+//             copies (a 2-stage ring per stream).  Writes the base-2
+//             log-sum-exp lse2[row, head] of x = logit * log2(e).  Its COLSUM
+//             form streams the keys the same way with the normalisers known and
+//             writes per-(row block, head) column sums for mutual scoring (Eq.
+//             mutual_scoring, every key takes the mean over rows);
+//             text_colsum_reduce adds them in a fixed order.
+// text_score  one workgroup per (sample, block of 128 keys, row block).  Each
+//             wave owns 32 keys.  For every head the 128 x d query tile is copied
+//             global -> LDS (double-buffered) and the wave's key fragments are
+//             loaded into registers one head ahead, while p = 2^(x - lse2) of the
+//             current head is accumulated over heads per (key, row).  Afterwards
+//             the row reduction of Eq. text_scoring is applied: max over rows for
+//             visual keys, mean for registers, both over the head mean (1/H); with
+//             several row blocks the per-block maxima and sums go through
+//             text_rows_combine.  Rows beyond T_b carry lse2 = +inf and so
+//             contribute exactly 0.
 //
 // The LDS copies are issued as inline global_load_lds so that the compiler does
 // not fold them into its own memory-counter waits; each kernel waits for them
 // explicitly (s_waitcnt vmcnt, then a barrier) before the stage is read.
 //
 // When the caller supplies its own natural-log normaliser (row_lse), text_stats
-// is skipped and text_score reads lse2 = row_lse * log2(e).
+// is skipped and the second pass reads lse2 = row_lse * log2(e).
 #include "occam_internal.hpp"
 
 namespace occam {

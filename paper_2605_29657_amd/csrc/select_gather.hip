@@ -3,13 +3,15 @@
 // Eqs. stage1 / stage2, the ascending compaction of the survivors, and the
 // dense copy of their rows that forms the pruned sequence of Algorithm 1.
 //
-// threshold    one thread per sample: tau = lambda * reduce(register scores).
+// threshold    one thread per sample: tau = lambda * reduce(register scores); for
+//              the ablation's mean-based threshold one workgroup per sample
+//              averages the visual scores instead (sample_reference).
 // select       one workgroup per sample: every thread owns a contiguous strip
 //              of candidates, counts the strip's survivors, a wave scan plus a
 //              4-entry LDS scan gives each strip its output position, and the
 //              strip writes its survivors' candidate-local indices, ascending,
 //              to the sample's slot of the workspace (slot[co_b + i]).
-//              Optionally computes tau first.
+//              Optionally computes tau first (fused threshold of occam_prune).
 // pack_gather  grid (G, sample): every workgroup forms its sample's packed
 //              offset (exclusive sum of the counts before it), writes the
 //              packed survivor list (through index_map when given) and
