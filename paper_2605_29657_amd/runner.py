@@ -34,7 +34,7 @@ class DeviceStage:
     """
 
     def __init__(self, sb: StageBatch, device="cuda", ragged=None, payload=True,
-                 softmax_scale: float = 0.0):
+                 softmax_scale: float = 0.0, max_cands=None):
         self.sb = sb
         self.device = device
         self.ragged = sb.ragged if ragged is None else bool(ragged)
@@ -51,7 +51,8 @@ class DeviceStage:
             self.k_off = _i32(sb.k_off, device)
             self.problem = occam.Problem(sb.B, sb.H, sb.Hkv, sb.d, sb.R, q_offsets=self.q_off,
                                          key_offsets=self.k_off, max_rows=int(sb.T.max()),
-                                         max_cands=int(sb.N.max()), dtype=sb.dtype,
+                                         max_cands=int(sb.N.max()) if max_cands is None
+                                         else int(max_cands), dtype=sb.dtype,
                                          softmax_scale=softmax_scale, visual_row_reduce=rr)
         else:
             self.q_off = self.k_off = None

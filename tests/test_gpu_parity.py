@@ -20,11 +20,11 @@ from parity import (RTOL, check_bookkeeping, check_rows, check_scores, check_sel
 pytestmark = pytest.mark.gpu
 
 
-def run_and_check(sb, lam, reduce=oracle.REG_MEAN, ragged=None, rows=True):
+def run_and_check(sb, lam, reduce=oracle.REG_MEAN, ragged=None, rows=True, max_cands=None):
     print("case: %s/%s B=%d R=%d H=%d Hkv=%d d=%d T=%s N=%s dtype=%s lam=%.6g ragged=%s" % (
         sb.workload, sb.stage, sb.B, sb.R, sb.H, sb.Hkv, sb.d, sb.T[:4], sb.N[:4], sb.dtype, lam,
         ragged), flush=True)
-    ds = DeviceStage(sb, ragged=ragged)
+    ds = DeviceStage(sb, ragged=ragged, max_cands=max_cands)
     ds.prune(lam, reduce=reduce, with_rows=rows)
     g = ds.host(with_rows=rows)
     o = oracle_prune(sb, lam, reduce=reduce)
