@@ -1,0 +1,44 @@
+"""Host-side helpers of bench.py (CPU only): the chained Stage II batch and the
+algorithmic byte counts the roofline figures are built on."""
+import numpy as np
+
+import bench
+from paper_2605_29657_amd import synth
+
+
+def test_chained_stage_keeps_registers_and_the_kept_rows_in_order():
+    txt = synth.make_stage("llava15", "txt", B=3)
+    R = txt.R
+    kept_idx = np.array([0, 5, 7, 2, 300, 575], dtype=np.int32)
+    kept_off = np.array([0, 3, 3, 6])                        # sample 1 keeps nothing
+    ch = bench.chained_stage(txt, kept_idx, kept_off)
+    assert list(ch.N) == [3, 0, 3]
+    assert list(ch.k_off) == [0, R + 3, 2 * R + 3, 3 * R + 6]
+    for b in range(3):
+        kb, ckb = txt.k_off[b], ch.k_off[b]
+        assert np.array_equal(ch.k[ckb:ckb + R], txt.k[kb:kb + R])            # registers
+        for i, v in enumerate(kept_idx[kept_off[b]:kept_off[b + 1]]):
+            assert np.array_equal(ch.k[ckb + R + i], txt.k[kb + R + v])
+    # Payload rows follow the same selection with each tensor's own layout.
+    co = np.concatenate([[0], np.cumsum(txt.N)])
+    cco = np.concatenate([[0], np.cumsum(ch.N)])
+    for pl, cpl in zip(txt.payload, ch.payload):
+        assert (cpl.pad_rows, cpl.row0) == (pl.pad_rows, pl.row0)
+        for b in range(3):
+            for i, v in enumerate(kept_idx[kept_off[b]:kept_off[b + 1]]):
+                src = co[b] + b * pl.pad_rows + pl.row0 + v
+                dst = cco[b] + b * cpl.pad_rows + cpl.row0 + i
+                assert np.array_equal(cpl.rows[dst], pl.rows[src])
+    assert ch.q is txt.q and np.array_equal(ch.T, txt.T)
+
+
+def test_stage_bytes_of_the_headline_image():
+    # Per LLaVA-NeXT image: Stage II keys 2884 x 32 x 128 bf16, 128 x 32 x 128 query
+    # rows, 4 B per score; 40 survivors gather 24 KB rows (read and write) plus 4 B each.
+    sb = synth.make_stage("llava_next", "txt", B=1)
+    got = bench.stage_bytes(sb, np.array([40]))
+    assert got["keys"] == 2884 * 32 * 128 * 2
+    assert got["q"] == 128 * 32 * 128 * 2
+    assert got["scores"] == 2884 * 4
+    assert got["gather"] == 2 * 40 * (4096 + 32 * 128 + 32 * 128) * 2 + 4 * 40
+    assert got["total"] == got["keys"] + got["q"] + got["scores"] + got["gather"]
