@@ -654,9 +654,19 @@ __global__ __launch_bounds__(256) void text_colsum_reduce_kernel(Prob p, const f
     const int nrb_max = (p.max_rows + kTxtRows - 1) / kTxtRows, nrb = (T + kTxtRows - 1) / kTxtRows;
     const size_t smax = (size_t)(p.R + p.max_cands);
     const float* pb = part + (size_t)b * nrb_max * p.H * smax + s;
+    // Up to 16 partials are loaded before they are added (in order): the loads do not
+    // depend on the running sum, so they are in flight together.
+    const int n = nrb * p.H;
     float acc = 0.f;
-    for (int rb = 0; rb < nrb; ++rb)
-        for (int h = 0; h < p.H; ++h) acc += pb[((size_t)rb * p.H + h) * smax];
+    int i = 0;
+    for (; i + 16 <= n; i += 16) {
+        float v[16];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) v[j] = pb[(size_t)(i + j) * smax];
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc += v[j];
+    }
+    for (; i < n; ++i) acc += pb[(size_t)i * smax];
     scores[k_begin(p, b) + s] = T > 0 ? acc * (1.f / ((float)p.H * (float)T)) : 0.f;
 }
 
