@@ -384,6 +384,40 @@ def score_source_sha256() -> str:
     return h.hexdigest()
 
 
+def traffic_from_counters(fetch_csv: str, write_csv: str, workload: str) -> dict:
+    """profiles/traffic.json from two rocprofv3 --pmc runs of `bench.py --kernel-only`.
+
+    FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of every text_score dispatch are averaged
+    and scaled by what the same counter reads for the run's last dispatch, the plain
+    1 GiB device copy (__amd_rocclr_copyBuffer) that --kernel-only ends with.
+    """
+    import csv
+
+    def read(path):
+        rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
+        score = [float(r["Counter_Value"]) for r in rows if "text_score_kernel" in r["Kernel_Name"]]
+        copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        if not score or not copy:
+            raise SystemExit("%s: no text_score or copy dispatch" % path)
+        return sum(score) / len(score), copy[-1], len(score)
+
+    gib_kib = float(1 << 20)
+    f_kib, f_copy, n_f = read(fetch_csv)
+    w_kib, w_copy, n_w = read(write_csv)
+    f_scale, w_scale = gib_kib / f_copy, gib_kib / w_copy
+    fetch = f_kib * f_scale * 1024.0
+    write = w_kib * w_scale * 1024.0
+    return {"kernel": "text_score", "workload": workload,
+            "bytes_per_launch": int(round(fetch + write)),
+            "fetch_bytes": int(round(fetch)), "write_bytes": int(round(write)),
+            "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
+            "dispatches": [n_f, n_w],
+            "source_sha256": score_source_sha256(),
+            "note": "FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of text_score, scaled by "
+                    "what the same counters read for a 1 GiB device copy; see "
+                    "text_score_traffic_llava_next.md"}
+
+
 def reference_lse(torch, txt, dt):
     """Per-(row, head) natural log-sum-exp of a uniform text stage, float32 on the device.
 
@@ -421,7 +455,17 @@ def main():
     ap.add_argument("--kernel-only", action="store_true",
                     help="run only the dominant kernel (and a plain 1 GiB device copy of known "
                          "size that calibrates byte counters), for counter collection")
+    ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="write profiles/traffic.json from the counter_collection.csv files "
+                         "of two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --kernel-only")
     args = ap.parse_args()
+    if args.traffic_from:
+        tj = traffic_from_counters(args.traffic_from[0], args.traffic_from[1], args.workload)
+        with open(os.path.join(ROOT, "profiles", "traffic.json"), "w") as f:
+            json.dump(tj, f, indent=1)
+            f.write("\n")
+        print(json.dumps(tj))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the pruning path is per sample and needs no "
               "communication; run it with --gpus 1 (see DESIGN.md for how it shards)",
