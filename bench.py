@@ -308,9 +308,19 @@ def stage_breakdown(torch, dv, dt, txt, lam1: float, lam2: float, steps: int) ->
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / n
 
+    from paper_2605_29657_amd import occam
+
     B = dv.sb.B
     ms1 = timed(lambda: dv.prune(lam1), steps)
     ms2 = timed(lambda: dt.prune(lam2), steps)
+    b1 = stage_bytes(dv.sb, dv.out["kept_count"].cpu().numpy())["total"]
+    b2 = stage_bytes(dt.sb, dt.out["kept_count"].cpu().numpy())["total"]
+    # Stage I scoring alone (occam_score: the one-row logits with online statistics, then
+    # the scores): reads every key once, writes one score per key.
+    sc1 = torch.empty_like(dv.out["scores"])
+    ms1s = timed(lambda: occam.score(dv.problem, dv.q, dv.k, sc1, dv.ws), steps)
+    e1 = 2 if dv.sb.dtype == "bf16" else 4
+    bs1 = int(dv.sb.k_off[-1]) * (dv.sb.Hkv * dv.sb.d * e1 + 4) + int(dv.sb.q_off[-1]) * dv.sb.H * dv.sb.d * e1
     kept_idx = dv.out["kept_idx"].cpu().numpy()
     kept_off = dv.out["kept_offsets"].cpu().numpy()
     ch = chained_stage(txt, kept_idx, kept_off)
@@ -319,7 +329,15 @@ def stage_breakdown(torch, dv, dt, txt, lam1: float, lam2: float, steps: int) ->
     ms2c = timed(lambda: dc.prune(lam2, index_map=imap), steps)
     kept2c = dc.out["kept_count"].float().mean().item()
     del dc
+    gbs = lambda nbytes, ms: nbytes / (ms * 1e-3) / 1e9
     return {"stage1_ms": round(ms1, 4), "stage2_ms": round(ms2, 4),
+            "stage1_hbm_gbs": round(gbs(b1, ms1), 1),
+            "stage1_hbm_frac": round(gbs(b1, ms1) / HBM_PEAK_GBS, 4),
+            "stage2_hbm_gbs": round(gbs(b2, ms2), 1),
+            "stage2_hbm_frac": round(gbs(b2, ms2) / HBM_PEAK_GBS, 4),
+            "stage1_score": {"ms": round(ms1s, 4), "bytes": bs1,
+                             "hbm_gbs": round(gbs(bs1, ms1s), 1),
+                             "hbm_frac": round(gbs(bs1, ms1s) / HBM_PEAK_GBS, 4)},
             "chained": {"stage2_keys_mean": float(np.mean(ch.N + ch.R)),
                         "stage2_ms": round(ms2c, 4), "step_ms": round(ms1 + ms2c, 4),
                         "images_s": round(B / ((ms1 + ms2c) * 1e-3), 1),
@@ -645,9 +663,12 @@ def main():
     rec["budget_matching"] = budget_matching_bench(torch)
     log("budget matching: %.1f us" % rec["budget_matching"]["us"])
     rec["stages"] = stage_breakdown(torch, dv, dt, txt, lam1, lam2, max(10, args.steps // 2))
-    log("stage I alone %.3f ms, stage II alone %.3f ms; chained step %.3f ms (%.0f keys)" % (
-        rec["stages"]["stage1_ms"], rec["stages"]["stage2_ms"], rec["stages"]["chained"]["step_ms"],
-        rec["stages"]["chained"]["stage2_keys_mean"]))
+    log("stage I alone %.3f ms (%.1f%% of HBM peak; its scoring %.1f%%), stage II alone %.3f ms "
+        "(%.1f%%); chained step %.3f ms (%.0f keys)" % (
+            rec["stages"]["stage1_ms"], 100 * rec["stages"]["stage1_hbm_frac"],
+            100 * rec["stages"]["stage1_score"]["hbm_frac"], rec["stages"]["stage2_ms"],
+            100 * rec["stages"]["stage2_hbm_frac"], rec["stages"]["chained"]["step_ms"],
+            rec["stages"]["chained"]["stage2_keys_mean"]))
     rec["ablation"] = ablation_steps(torch, dv, dt, float(kept1.mean()), float(kept2.mean()),
                                      max(10, args.steps // 2))
     log("ablation: mean threshold %.3f ms/step, fixed budget %.3f ms/step" % (

@@ -42,3 +42,33 @@ def test_stage_bytes_of_the_headline_image():
     assert got["scores"] == 2884 * 4
     assert got["gather"] == 2 * 40 * (4096 + 32 * 128 + 32 * 128) * 2 + 4 * 40
     assert got["total"] == got["keys"] + got["q"] + got["scores"] + got["gather"]
+
+
+def _counter_csv(path, rows):
+    import csv
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"])
+        w.writeheader()
+        for i, (name, counter, value) in enumerate(rows):
+            w.writerow({"Dispatch_Id": i + 1, "Kernel_Name": name, "Counter_Name": counter,
+                        "Counter_Value": value})
+
+
+def test_traffic_from_counters_scales_by_the_calibration_copy(tmp_path):
+    # Two scoring dispatches and a 1 GiB copy whose FETCH_SIZE reads half its bytes: the
+    # kernel's fetch is doubled, its write kept; the earlier copyBuffer dispatches are set-up.
+    score = "void occam::text_score_kernel<8, false>(occam::Prob, ...)"
+    copy = "__amd_rocclr_copyBuffer"
+    fetch = tmp_path / "fetch.csv"
+    write = tmp_path / "write.csv"
+    _counter_csv(fetch, [(copy, "FETCH_SIZE", 7.0), (score, "FETCH_SIZE", 1000.0),
+                         (score, "FETCH_SIZE", 1200.0), (copy, "FETCH_SIZE", 524288.0)])
+    _counter_csv(write, [(copy, "WRITE_SIZE", 9.0), (score, "WRITE_SIZE", 10.0),
+                         (score, "WRITE_SIZE", 14.0), (copy, "WRITE_SIZE", 1048576.0)])
+    tj = bench.traffic_from_counters(str(fetch), str(write), "llava_next")
+    assert tj["fetch_scale"] == 2.0 and tj["write_scale"] == 1.0
+    assert tj["fetch_bytes"] == 1100 * 2 * 1024
+    assert tj["write_bytes"] == 12 * 1024
+    assert tj["bytes_per_launch"] == tj["fetch_bytes"] + tj["write_bytes"]
+    assert tj["dispatches"] == [2, 2]
+    assert tj["source_sha256"] == bench.score_source_sha256()
