@@ -39,7 +39,7 @@ def log(*a):
 
 
 def stage_bytes(sb, kept_per_sample) -> dict:
-    """Algorithmic HBM bytes of one fused prune over a batch (per-image figures in the design doc).
+    """Algorithmic HBM bytes of one fused prune over a batch.
 
     keys: every key row once; queries once; scores written once (4 B per key);
     gather: each survivor row read and written once; survivor lists 4 B each.
@@ -485,9 +485,9 @@ def main():
         print(json.dumps(tj))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the pruning path is per sample and needs no "
-              "communication; run it with --gpus 1 (see DESIGN.md for how it shards)",
-              file=sys.stderr)
+        print("bench.py measures one GPU: every sample is pruned independently, so a batch "
+              "shards across GPUs with no exchange and this build runs and measures one; "
+              "run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch
