@@ -436,6 +436,56 @@ def traffic_from_counters(fetch_csv: str, write_csv: str, workload: str) -> dict
                     "text_score_traffic_llava_next.md"}
 
 
+# Kernels of one headline step, in launch order: Stage I prune, then Stage II prune.
+STEP_KERNELS = [
+    ("cls_stream_kernel<true, 8, 2>", "cls_stream (Stage I logits + online statistics)"),
+    ("cls_scores_kernel<true>", "cls_scores (Stage I scores)"),
+    ("select_kernel", "select (Stage I)"),
+    ("pack_gather_kernel", "pack_gather (Stage I: 1024-wide hidden rows)"),
+    ("text_stats_kernel<8, false, false, 2>", "text_stats (Stage II normalisers)"),
+    ("text_score_kernel<8, false>", "text_score (Stage II scoring)"),
+    ("select_kernel", "select (Stage II)"),
+    ("pack_gather_kernel", "pack_gather (Stage II: hidden, K and V rows)"),
+]
+
+
+def trace_summary(trace_csv: str, warmup: int = 5, steps: int = 20) -> dict:
+    """Per-kernel durations of the headline step from a rocprofv3 --kernel-trace CSV of
+    `bench.py --steps N`: the first warmup + steps occurrences of the step's kernel
+    sequence (other launches in between are skipped), timed steps only; and the scoring
+    kernel alone, the first `steps` of its launches after a warm-up that follow the
+    steps (the roofline measurement's loop)."""
+    import csv
+    import re
+    import statistics as st
+
+    rows = sorted(csv.DictReader(open(trace_csv)), key=lambda r: int(r["Start_Timestamp"]))
+    short = [re.sub(r"\(.*", "", r["Kernel_Name"]).replace("void ", "").replace("occam::", "")
+             for r in rows]
+    dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
+    names = [k for k, _ in STEP_KERNELS]
+    ours = [i for i, n in enumerate(short) if not n.startswith(("at::", "__amd", "Cijk"))]
+    reps, j = [], 0
+    while j + len(names) <= len(ours) and len(reps) < warmup + steps:
+        if [short[i] for i in ours[j:j + len(names)]] == names:
+            reps.append([dur[i] for i in ours[j:j + len(names)]])
+            last = ours[j + len(names) - 1]
+            j += len(names)
+        else:
+            j += 1
+    if len(reps) < warmup + steps:
+        raise SystemExit("%s: found %d of %d steps" % (trace_csv, len(reps), warmup + steps))
+    timed = reps[warmup:]
+    per = [{"kernel": label, "avg_us": round(st.mean(r[k] for r in timed), 1),
+            "min_us": round(min(r[k] for r in timed), 1),
+            "max_us": round(max(r[k] for r in timed), 1)} for k, (_, label) in enumerate(STEP_KERNELS)]
+    alone = [dur[i] for i, n in enumerate(short) if n == "text_score_kernel<8, false>" and i > last]
+    alone = alone[1:1 + steps]
+    return {"steps": per, "step_sum_us": round(sum(x["avg_us"] for x in per), 1),
+            "text_score_alone": {"n": len(alone), "avg_us": round(st.mean(alone), 1),
+                                 "min_us": round(min(alone), 1), "max_us": round(max(alone), 1)}}
+
+
 def reference_lse(torch, txt, dt):
     """Per-(row, head) natural log-sum-exp of a uniform text stage, float32 on the device.
 
@@ -476,7 +526,13 @@ def main():
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic.json from the counter_collection.csv files "
                          "of two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --kernel-only")
+    ap.add_argument("--trace-summary", metavar="TRACE_CSV",
+                    help="per-kernel durations of the step from the kernel_trace.csv of a "
+                         "rocprofv3 --kernel-trace run of `bench.py --steps K` (K = --steps)")
     args = ap.parse_args()
+    if args.trace_summary:
+        print(json.dumps(trace_summary(args.trace_summary, args.warmup, args.steps), indent=1))
+        return
     if args.traffic_from:
         tj = traffic_from_counters(args.traffic_from[0], args.traffic_from[1], args.workload)
         with open(os.path.join(ROOT, "profiles", "traffic.json"), "w") as f:

@@ -72,3 +72,33 @@ def test_traffic_from_counters_scales_by_the_calibration_copy(tmp_path):
     assert tj["bytes_per_launch"] == tj["fetch_bytes"] + tj["write_bytes"]
     assert tj["dispatches"] == [2, 2]
     assert tj["source_sha256"] == bench.score_source_sha256()
+
+
+def test_trace_summary_finds_the_step_sequence_and_the_lone_scoring_loop(tmp_path):
+    import csv
+    names = [k for k, _ in bench.STEP_KERNELS]
+    rows, t = [], 0
+
+    def launch(name, us):
+        nonlocal t
+        rows.append({"Kernel_Name": "void occam::%s(occam::Prob, ...)" % name,
+                     "Start_Timestamp": t, "End_Timestamp": t + int(us * 1000)})
+        t += int(us * 1000) + 500
+
+    launch("at::native::fill", 3.0)                    # set-up work is skipped
+    for rep in range(25):                              # 5 warm-up + 20 timed steps
+        for k, n in enumerate(names):
+            launch(n, 10.0 * (k + 1) + (rep >= 5) * 1.0)
+        if rep == 7:
+            launch("at::native::copy", 2.0)
+    for i in range(21):                                # one warm-up + 20 timed, alone
+        launch("text_score_kernel<8, false>", 200.0 + i)
+    path = tmp_path / "trace.csv"
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
+        w.writeheader()
+        w.writerows(rows)
+    got = bench.trace_summary(str(path), warmup=5, steps=20)
+    assert [x["avg_us"] for x in got["steps"]] == [10.0 * (k + 1) + 1.0 for k in range(8)]
+    assert got["text_score_alone"]["n"] == 20
+    assert got["text_score_alone"]["min_us"] == 201.0 and got["text_score_alone"]["max_us"] == 220.0
