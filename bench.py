@@ -411,12 +411,12 @@ def traffic_from_counters(fetch_csv: str, write_csv: str, workload: str) -> dict
     """
     import csv
 
-    def read(path):
+    def read(path, kernel="text_score_kernel"):
         rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
-        score = [float(r["Counter_Value"]) for r in rows if "text_score_kernel" in r["Kernel_Name"]]
+        score = [float(r["Counter_Value"]) for r in rows if kernel in r["Kernel_Name"]]
         copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
         if not score or not copy:
-            raise SystemExit("%s: no text_score or copy dispatch" % path)
+            raise SystemExit("%s: no %s or copy dispatch" % (path, kernel))
         return sum(score) / len(score), copy[-1], len(score)
 
     gib_kib = float(1 << 20)
@@ -425,7 +425,16 @@ def traffic_from_counters(fetch_csv: str, write_csv: str, workload: str) -> dict
     f_scale, w_scale = gib_kib / f_copy, gib_kib / w_copy
     fetch = f_kib * f_scale * 1024.0
     write = w_kib * w_scale * 1024.0
-    return {"kernel": "text_score", "workload": workload,
+    extra = {}
+    try:
+        cf, _, n_c = read(fetch_csv, "cls_stream_kernel")
+        cw, _, _ = read(write_csv, "cls_stream_kernel")
+        extra = {"cls_stream": {"fetch_bytes": int(round(cf * f_scale * 1024.0)),
+                                "write_bytes": int(round(cw * w_scale * 1024.0)),
+                                "dispatches": n_c}}
+    except SystemExit:
+        pass
+    return {**{"kernel": "text_score", "workload": workload,
             "bytes_per_launch": int(round(fetch + write)),
             "fetch_bytes": int(round(fetch)), "write_bytes": int(round(write)),
             "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4),
@@ -433,7 +442,7 @@ def traffic_from_counters(fetch_csv: str, write_csv: str, workload: str) -> dict
             "source_sha256": score_source_sha256(),
             "note": "FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of text_score, scaled by "
                     "what the same counters read for a 1 GiB device copy; see "
-                    "text_score_traffic_llava_next.md"}
+                    "text_score_traffic_llava_next.md"}, **extra}
 
 
 # Kernels of one headline step, in launch order: Stage I prune, then Stage II prune.
@@ -574,13 +583,19 @@ def main():
             occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws, row_lse=lse)
         for _ in range(args.kernel_reps):
             occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws)     # statistics + scoring
+        # Stage I scoring (the one-row logits with online statistics, then the scores).
+        vis = synth.make_stage(name, "vis", payload=False)
+        dv = DeviceStage(vis, ragged=vis.ragged, payload=False)
+        vis_scores = torch.empty_like(dv.out["scores"])
+        for _ in range(args.kernel_reps):
+            occam.score(dv.problem, dv.q, dv.k, vis_scores, dv.ws)
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
         dst = torch.empty_like(src)
         src.fill_(1)
         dst.copy_(src)
         torch.cuda.synchronize()
         log("kernel-only: %d launches of text_score alone, %d of text_stats + text_score, "
-            "one 1 GiB device copy" % (args.kernel_reps, args.kernel_reps))
+            "%d of the Stage I scoring, one 1 GiB device copy" % ((args.kernel_reps,) * 3))
         return
     vis = synth.make_stage(name, "vis")
     txt = synth.make_stage(name, "txt")
