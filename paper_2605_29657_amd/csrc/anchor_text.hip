@@ -12,13 +12,12 @@
 // Every (row, head) softmax needs its normaliser before the head mean can be
 // formed, so the path has two passes over the keys:
 //
-// text_stats  task (sample, head, row block of 128), XCD-aware.  Key streams of
-//             two waves x 64 rows (one row block) or four waves x 32 rows (rows
-//             spanning several blocks); each stream owns every kStreams-th block
-//             of 32 keys, the query rows of the head sit in registers as MFMA B
-//             fragments, and an online (max, sum 2^x) pair is kept per row;
-//             pairs are merged across the two lane halves and the streams in a
-//             fixed order.  Key blocks reach LDS through direct global -> LDS
+// text_stats  task (sample, head, row block of 128), XCD-aware.  One key stream
+//             consumed by four waves of 32 rows (the kernel also has a two-stream
+//             form of two 64-row waves each); the query rows of the head sit in
+//             registers as MFMA B fragments, and an online (max, sum 2^x) pair is
+//             kept per row; pairs are merged across the two lane halves (and
+//             streams) in a fixed order.  Key blocks reach LDS through direct global -> LDS
 //             copies (a 2-stage ring per stream).  Writes the base-2
 //             log-sum-exp lse2[row, head] of x = logit * log2(e).  Its COLSUM
 //             form streams the keys the same way with the normalisers known and
@@ -127,7 +126,7 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     // consume the same key blocks, so each block is copied once per stream, global ->
     // LDS, into a ring of kStatsRing stages per stream: kStatsRing - 1 blocks are in
     // flight while one is used.  RG = 4 (32 rows per wave) needs half the registers of
-    // RG = 2 and runs more waves per SIMD; it is used when the rows span several blocks.
+    // RG = 2 and runs more waves per SIMD; the launcher uses it for every row count.
     // A block is 32 keys x NCH 16-byte chunks; chunk c of key j sits in LDS unit
     // j*NCH + (c ^ (j & SW)), SW = NCH - 1 when NCH is a power of two (else 0), so a
     // copy writes whole 256-byte key slices and the MFMA fragment reads of 32
@@ -622,14 +621,13 @@ static hipError_t stats_launch_rg(const Prob& p, const void* q, const void* k, f
     return hipGetLastError();
 }
 
-// Rows spanning several 128-row blocks (long anchor sets, mutual scoring): four waves
-// of 32 rows per key stream; one block: two waves of 64 rows per stream.
+// Four waves of 32 rows on one key stream.  Two streams of two 64-row waves reuse each
+// key fragment twice per wave but need twice the registers; at one 128-row block (T =
+// 128, LLaVA-NeXT) the one-stream form measured 6 % faster (137-139 against 146-147 us).
 template <int DS, bool HALF, bool COLSUM>
 static hipError_t stats_launch(const Prob& p, const void* q, const void* k, float* lse2,
                                const float* lse_in, int lse_natural, float* part, hipStream_t s) {
-    if (p.max_rows > kTxtRows)
-        return stats_launch_rg<DS, HALF, COLSUM, 4>(p, q, k, lse2, lse_in, lse_natural, part, s);
-    return stats_launch_rg<DS, HALF, COLSUM, 2>(p, q, k, lse2, lse_in, lse_natural, part, s);
+    return stats_launch_rg<DS, HALF, COLSUM, 4>(p, q, k, lse2, lse_in, lse_natural, part, s);
 }
 
 template <int DS, bool HALF>
