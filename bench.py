@@ -451,7 +451,7 @@ STEP_KERNELS = [
     ("cls_scores_kernel<true>", "cls_scores (Stage I scores)"),
     ("select_kernel", "select (Stage I)"),
     ("pack_gather_kernel", "pack_gather (Stage I: 1024-wide hidden rows)"),
-    ("text_stats_kernel<8, false, false, 2>", "text_stats (Stage II normalisers)"),
+    ("text_stats_kernel<8, false, false, 4>", "text_stats (Stage II normalisers)"),
     ("text_score_kernel<8, false>", "text_score (Stage II scoring)"),
     ("select_kernel", "select (Stage II)"),
     ("pack_gather_kernel", "pack_gather (Stage II: hidden, K and V rows)"),
