@@ -62,11 +62,12 @@ __device__ __forceinline__ float reg_reduce(const float* s, int R, int reduce) {
 
 constexpr int kRefCandMean = 3;            // OCCAM_REF_CAND_MEAN
 
-// Reference score of sample b, returned to every thread of a workgroup of NT threads
-// (all of them must call it).  Register reductions read the R register scores; the
-// candidate mean sums the visual scores in a fixed order (strided per thread, a fixed
-// shuffle tree per wave, the waves in order), so every kernel that calls it with the
-// same NT gets the same bits.  `red` is NT / 64 floats of LDS.
+// Reference score of sample b, returned to every thread of a workgroup of at least NT
+// threads (all of them must call it).  Register reductions read the R register scores;
+// the candidate mean sums the visual scores in a fixed order (strided over the first NT
+// threads, a fixed shuffle tree per wave, the waves in order; threads past NT take no
+// part), so every kernel that calls it with the same NT gets the same bits, whatever
+// its workgroup size.  `red` is NT / 64 floats of LDS.
 template <int NT>
 __device__ __forceinline__ float sample_reference(const Prob& p, const float* scores, int b,
                                                   int reduce, float* red) {
@@ -74,12 +75,14 @@ __device__ __forceinline__ float sample_reference(const Prob& p, const float* sc
     if (reduce != kRefCandMean) return reg_reduce(scores + kb, p.R, reduce);
     const int N = keys_of(p, b) - p.R;
     const float* sv = scores + kb + p.R;
+    const bool part = threadIdx.x < NT;
     float acc = 0.f;
-    for (int v = threadIdx.x; v < N; v += NT) acc += sv[v];
+    if (part)
+        for (int v = threadIdx.x; v < N; v += NT) acc += sv[v];
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
     __syncthreads();                          // `red` may still be read by a previous call
-    if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
+    if (part && (threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = acc;
     __syncthreads();
     float sum = 0.f;
 #pragma unroll
@@ -127,7 +130,8 @@ constexpr int kScoreThreads = 256;
 constexpr int kTxtRows = 128;
 constexpr int kTxtKeysPerWave = 32;
 constexpr int kTxtKeysPerWg = 128;   // score kernel: 4 key blocks of 32
-constexpr int kSelThreads = 256;
+constexpr int kSelThreads = 256;    // threshold, top-K, budget matching; reference-sum order
+constexpr int kSelectThreads = 512; // the select kernel (its reference sum uses kSelThreads)
 constexpr int kGatherThreads = 256;
 
 // The chip dispatches consecutive workgroups of a launch round-robin over its 8
