@@ -15,8 +15,11 @@
 // text_stats  task (sample, head, row block of 128), XCD-aware.  One key stream
 //             consumed by four waves of 32 rows (the kernel also has a two-stream
 //             form of two 64-row waves each); the query rows of the head sit in
-//             registers as MFMA B fragments, and an online (max, sum 2^x) pair is
-//             kept per row; pairs are merged across the two lane halves (and
+//             registers as MFMA B fragments, and a (reference, sum 2^(x - reference))
+//             pair is kept per row: the reference is the first key block's maximum
+//             and moves only when a block's sum would exceed 2^64, so a logit costs
+//             a multiply-add, an exponential and an add (no running maximum); pairs
+//             are merged across the two lane halves (and
 //             streams) in a fixed order.  Key blocks reach LDS through direct global -> LDS
 //             copies (a 2-stage ring per stream).  Writes the base-2
 //             log-sum-exp lse2[row, head] of x = logit * log2(e).  Its COLSUM
@@ -242,8 +245,13 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     // reads (kfrag ^ kk*32) with SW, (kfrag + kk*32) without.
     const uint32_t kfrag = (uint32_t)(lo * NCH + (hi ^ (lo & SW))) * 16u;
 
-    // One key block: MFMA logits from the LDS stage, then the online (max, sum) update.
-    auto block = [&](int kbi, const u32x4* blk) -> float {
+    // One key block: MFMA logits from the LDS stage, then the (reference, sum) update.
+    // The reference m of a row is the largest logit of the wave's first block (all later
+    // blocks see a full first block, so m is finite there).  Later blocks add
+    // 2^(x - m) with m fixed; x may exceed m, and a block whose sum passes 2^64 (or
+    // overflows) is redone with its own maximum, which also moves m.  Terms below
+    // 2^-126 relative to m are below float32 resolution of z >= 1.
+    auto block = [&](int kbi, const u32x4* blk, bool first) -> float {
         const int nvalid = S - kbi * 32;
         u32x4 kf[DS];
 #pragma unroll
@@ -285,6 +293,22 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
 #pragma unroll
         for (int sb = 0; sb < NSBW; ++sb) {
             if (sb >= nsb) break;
+            if (!first) {
+                // Sum against the fixed reference in four partial chains (r mod 4).
+                float a4[4] = {0.f, 0.f, 0.f, 0.f};
+                if (nvalid >= 32) {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        a4[r & 3] += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -m[sb]));
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 16; ++r)
+                        if (acc_key(r, hi) < nvalid)
+                            a4[r & 3] += __builtin_amdgcn_exp2f(fmaf(acc[sb][r], c2, -m[sb]));
+                }
+                const float asum = (a4[0] + a4[1]) + (a4[2] + a4[3]);
+                if (asum <= 0x1p64f) { z[sb] += asum; continue; }
+            }
             // Maximum and sum over the lane's 16 keys in four partial chains (r mod 4).
             float m4[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
             if (nvalid >= 32) {
@@ -345,7 +369,7 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
         if (COLSUM && rg == 0 && i >= 1 && i - 1 < nmine) store_sums(i - 1);
         if (i < nmine) {
             float cs = 0.f;
-            if (nsb > 0) cs = block(ks + i * kStreams, sring + (i % kStatsRing) * UNITS);
+            if (nsb > 0) cs = block(ks + i * kStreams, sring + (i % kStatsRing) * UNITS, i == 0);
             if (COLSUM && hi == 0) sums[((i & 1) * kStreams + ks) * (RG * 32) + rg * 32 + lo] = cs;
         }
     }

@@ -195,6 +195,26 @@ def test_lambda_zero_keeps_everything_and_huge_keeps_nothing():
     assert np.all(g["kept_count"] == 0) and np.all(g["kept_offsets"] == 0)
 
 
+def test_late_keys_far_above_the_early_ones():
+    # Sinks scaled x25 and x60 put some (row, head) logits 2^64 .. 2^128 and more than
+    # 2^128 (in base-2 units) above the largest logit among the sample's first 32 keys:
+    # sums against an early reference would overflow float32, so the statistics pass
+    # must re-reference those rows.
+    for scale, seed in ((25.0, 3), (60.0, 4)):
+        sb = custom_stage(B=2, R=4, H=8, Hkv=8, d=128, T=[128, 60], N=[700, 300], sinks=6,
+                          sink_scale=scale, seed=seed)
+        q, k = synth.bf16_bits_to_f32(sb.q), synth.bf16_bits_to_f32(sb.k)
+        gaps = []
+        for b in range(sb.B):
+            qb = q[sb.q_off[b]:sb.q_off[b + 1]].astype(np.float64)
+            kb = k[sb.k_off[b]:sb.k_off[b + 1]].astype(np.float64)
+            x = np.einsum("thd,shd->hts", qb, kb) / np.sqrt(sb.d) * np.log2(np.e)
+            gaps.append((x.max(axis=2) - x[:, :, :32].max(axis=2)).ravel())
+        gaps = np.concatenate(gaps)
+        assert np.any((gaps > 64) & (gaps < 128)) and np.any(gaps > 128), (scale, gaps.max())
+        run_and_check(sb, 1.0)
+
+
 @pytest.mark.parametrize("reduce", [oracle.REG_MAX, oracle.REG_SUM])
 def test_other_register_reductions(reduce):
     sb = custom_stage(B=2, R=8, H=8, Hkv=8, d=64, T=[1, 1], N=[500, 333])
