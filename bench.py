@@ -452,7 +452,7 @@ STEP_KERNELS = [
     ("select_kernel", "select (Stage I)"),
     ("pack_gather_kernel", "pack_gather (Stage I: 1024-wide hidden rows)"),
     ("text_stats_kernel<8, false, false, 4>", "text_stats (Stage II normalisers)"),
-    ("text_score_kernel<8, false>", "text_score (Stage II scoring)"),
+    ("text_score_kernel<8, false, true>", "text_score (Stage II scoring)"),
     ("select_kernel", "select (Stage II)"),
     ("pack_gather_kernel", "pack_gather (Stage II: hidden, K and V rows)"),
 ]
@@ -488,7 +488,7 @@ def trace_summary(trace_csv: str, warmup: int = 5, steps: int = 20) -> dict:
     per = [{"kernel": label, "avg_us": round(st.mean(r[k] for r in timed), 1),
             "min_us": round(min(r[k] for r in timed), 1),
             "max_us": round(max(r[k] for r in timed), 1)} for k, (_, label) in enumerate(STEP_KERNELS)]
-    alone = [dur[i] for i, n in enumerate(short) if n == "text_score_kernel<8, false>" and i > last]
+    alone = [dur[i] for i, n in enumerate(short) if n == "text_score_kernel<8, false, true>" and i > last]
     alone = alone[1:1 + steps]
     return {"steps": per, "step_sum_us": round(sum(x["avg_us"] for x in per), 1),
             "text_score_alone": {"n": len(alone), "avg_us": round(st.mean(alone), 1),

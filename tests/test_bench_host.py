@@ -57,7 +57,7 @@ def _counter_csv(path, rows):
 def test_traffic_from_counters_scales_by_the_calibration_copy(tmp_path):
     # Two scoring dispatches and a 1 GiB copy whose FETCH_SIZE reads half its bytes: the
     # kernel's fetch is doubled, its write kept; the earlier copyBuffer dispatches are set-up.
-    score = "void occam::text_score_kernel<8, false>(occam::Prob, ...)"
+    score = "void occam::text_score_kernel<8, false, true>(occam::Prob, ...)"
     copy = "__amd_rocclr_copyBuffer"
     fetch = tmp_path / "fetch.csv"
     write = tmp_path / "write.csv"
@@ -92,7 +92,7 @@ def test_trace_summary_finds_the_step_sequence_and_the_lone_scoring_loop(tmp_pat
         if rep == 7:
             launch("at::native::copy", 2.0)
     for i in range(21):                                # one warm-up + 20 timed, alone
-        launch("text_score_kernel<8, false>", 200.0 + i)
+        launch("text_score_kernel<8, false, true>", 200.0 + i)
     path = tmp_path / "trace.csv"
     with open(path, "w", newline="") as f:
         w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
