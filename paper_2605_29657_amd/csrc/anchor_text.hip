@@ -401,6 +401,51 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     }
 }
 
+// Ragged launches: workgroup id -> the id-th non-empty (sample, key chunk, row block)
+// task of the scoring pass, so that the active tasks take the lowest ids and spread over
+// the CUs in dispatch order, instead of sitting among the empty chunks of short samples
+// (where two of them can share a CU while other CUs idle).  Samples in reverse order,
+// chunks then row blocks, as in the uniform mapping; xcd_remap over the A active tasks
+// keeps a sample's tasks on one XCD.  Called by wave 0: each lane counts the tasks of a
+// run of consecutive samples, a scan finds the lane and sample holding the task, which
+// leaves (b, c, rb) in sh[0..2], or b = -1 past the last task.
+__device__ void ragged_score_task(const Prob& p, int id, int* sh) {
+    const int lane = threadIdx.x;
+    const int per = (p.B + kWave - 1) / kWave;
+    const int i0 = min(lane * per, p.B), i1 = min(i0 + per, p.B);
+    auto ntask = [&](int b) {
+        const int T = rows_of(p, b), S = keys_of(p, b);
+        if (T <= 0 || S <= 0) return 0;
+        return ((S + kTxtKeysPerWg - 1) / kTxtKeysPerWg) * ((T + kTxtRows - 1) / kTxtRows);
+    };
+    int cnt = 0;
+    for (int i = i0; i < i1; ++i) cnt += ntask(p.B - 1 - i);
+    int incl = cnt;
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int v = __shfl_up(incl, off);
+        if (lane >= off) incl += v;
+    }
+    const int A = __shfl(incl, kWave - 1);
+    if (id >= A) {
+        if (lane == 0) sh[0] = -1;
+        return;
+    }
+    const int t = xcd_remap(id, A);
+    int acc = incl - cnt;
+    if (t < acc || t >= incl) return;
+    for (int i = i0; i < i1; ++i) {
+        const int b = p.B - 1 - i, n = ntask(b);
+        if (t < acc + n) {
+            const int nrb_b = (rows_of(p, b) + kTxtRows - 1) / kTxtRows;
+            sh[0] = b;
+            sh[1] = (t - acc) / nrb_b;
+            sh[2] = (t - acc) % nrb_b;
+            return;
+        }
+        acc += n;
+    }
+}
+
 template <int DS, bool HALF, bool FULL>
 __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -436,8 +481,23 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     // and text_rows_combine forms the scores.
     const int nchunk = (p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg;
     const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
-    const int task = xcd_remap((int)blockIdx.x, nchunk * nrb * p.B);
-    const int rb = task % nrb, c = (task / nrb) % nchunk, b = p.B - 1 - task / (nrb * nchunk);
+    int b, c, rb;
+    if (p.k_off || p.q_off) {
+        // The decoded task passes through the start of query buffer 1, which is first
+        // written (head 1's copy) after the barrier that ends the prologue.
+        int* sh = reinterpret_cast<int*>(qt + QTILE);
+        if (threadIdx.x < kWave) ragged_score_task(p, (int)blockIdx.x, sh);
+        __syncthreads();
+        b = sh[0];
+        if (b < 0) return;
+        c = sh[1];
+        rb = sh[2];
+    } else {
+        const int task = xcd_remap((int)blockIdx.x, nchunk * nrb * p.B);
+        rb = task % nrb;
+        c = (task / nrb) % nchunk;
+        b = p.B - 1 - task / (nrb * nchunk);
+    }
     const int S = keys_of(p, b);
     const int s_lo = c * kTxtKeysPerWg;
     const int t0 = rb * kTxtRows;
