@@ -195,6 +195,18 @@ def test_lambda_zero_keeps_everything_and_huge_keeps_nothing():
     assert np.all(g["kept_count"] == 0) and np.all(g["kept_offsets"] == 0)
 
 
+def test_ragged_text_with_many_samples():
+    # 130 ragged samples: each lane of the task-decoding wave counts three samples, some
+    # samples have no candidates, some rows span two 128-row blocks.
+    rng = np.random.default_rng(11)
+    B = 130
+    T = rng.integers(1, 200, size=B)
+    N = rng.integers(0, 300, size=B)
+    N[::17] = 0
+    sb = custom_stage(B=B, R=4, H=4, Hkv=4, d=64, T=list(T), N=list(N), seed=5)
+    run_and_check(sb, 1.0)
+
+
 def test_late_keys_far_above_the_early_ones():
     # Sinks scaled x25 and x60 put some (row, head) logits 2^64 .. 2^128 and more than
     # 2^128 (in base-2 units) above the largest logit among the sample's first 32 keys:
