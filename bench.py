@@ -391,6 +391,18 @@ def workload_step(torch, name: str, steps: int) -> dict:
     return out
 
 
+def step_desc(name, vis, txt) -> str:
+    """The headline step's workload in words, from the two stage batches (ranges for ragged
+    sizes)."""
+    def rng(a):
+        lo, hi = int(np.min(a)), int(np.max(a))
+        return "%d" % lo if lo == hi else "%d-%d" % (lo, hi)
+    return ("%s: B=%d, R=%d, N=%s visual tokens; Stage I CLS row H=%d d=%d + %d-wide hidden gather; "
+            "Stage II %s text rows H=%d d=%d over all %s tokens + hidden/K/V gather" % (
+                name, vis.B, vis.R, rng(vis.N), vis.H, vis.d, vis.payload[0].rows.shape[1],
+                rng(txt.T), txt.H, txt.d, rng(txt.N)))
+
+
 def score_source_sha256() -> str:
     """sha256 of the sources the Stage II scoring kernel is built from."""
     import hashlib
@@ -708,10 +720,7 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": "%s: B=%d, R=%d, N=%d visual tokens; Stage I CLS row H=16 d=64 "
-                               "+ 1024-wide hidden gather; Stage II %d text rows H=32 d=128 over "
-                               "all %d tokens + hidden/K/V gather" % (
-                                   name, B, w["R"], w["N"], w["txt"]["T"], w["N"]),
+        "config": {"workload": step_desc(name, vis, txt),
                    "global_batch": B, "lambda1": lam1, "lambda2": lam2,
                    "kept_stage1_mean": float(np.mean(kept1)),
                    "kept_stage2_mean": float(np.mean(kept2))},

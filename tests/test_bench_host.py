@@ -102,3 +102,19 @@ def test_trace_summary_finds_the_step_sequence_and_the_lone_scoring_loop(tmp_pat
     assert [x["avg_us"] for x in got["steps"]] == [10.0 * (k + 1) + 1.0 for k in range(8)]
     assert got["text_score_alone"]["n"] == 20
     assert got["text_score_alone"]["min_us"] == 201.0 and got["text_score_alone"]["max_us"] == 220.0
+
+
+def test_step_description_covers_ragged_workloads():
+    # The bench line's workload text for a ragged batch gives ranges (it used to format a
+    # range as one integer and fail); the uniform headline text is unchanged.
+    from paper_2605_29657_amd import synth
+    v = synth.make_stage("qwen3vl_ragged", "vis", B=3)
+    t = synth.make_stage("qwen3vl_ragged", "txt", B=3)
+    desc = bench.step_desc("qwen3vl_ragged", v, t)
+    assert "N=%d-%d visual tokens" % (v.N.min(), v.N.max()) in desc
+    assert "d=72" in desc and "1152-wide hidden" in desc
+    v = synth.make_stage("llava_next", "vis", B=2)
+    t = synth.make_stage("llava_next", "txt", B=2)
+    assert bench.step_desc("llava_next", v, t) == (
+        "llava_next: B=2, R=4, N=2880 visual tokens; Stage I CLS row H=16 d=64 + 1024-wide hidden "
+        "gather; Stage II 128 text rows H=32 d=128 over all 2880 tokens + hidden/K/V gather")
