@@ -324,7 +324,8 @@ def stage_breakdown(torch, dv, dt, txt, lam1: float, lam2: float, steps: int) ->
     kept_idx = dv.out["kept_idx"].cpu().numpy()
     kept_off = dv.out["kept_offsets"].cpu().numpy()
     ch = chained_stage(txt, kept_idx, kept_off)
-    dc = DeviceStage(ch, ragged=True)
+    # Every sample keeps its T text rows; only the key counts are ragged.
+    dc = DeviceStage(ch, ragged=True, row_offsets=not bool(np.all(ch.T == ch.T[0])))
     imap = dv.out["kept_idx"][:int(kept_off[-1])].clone()
     ms2c = timed(lambda: dc.prune(lam2, index_map=imap), steps)
     kept2c = dc.out["kept_count"].float().mean().item()

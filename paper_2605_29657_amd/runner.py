@@ -30,11 +30,13 @@ class DeviceStage:
     """One stage of a batch resident in HBM, ready for the library's calls.
 
     ``ragged``: pass device offsets (True) or the uniform shape (False); defaults to
-    whether the batch actually is ragged.
+    whether the batch actually is ragged.  ``row_offsets`` (ragged only): False passes the
+    key offsets alone, with the uniform row count, for batches whose samples all have the
+    same number of anchor rows; None or True passes both.
     """
 
     def __init__(self, sb: StageBatch, device="cuda", ragged=None, payload=True,
-                 softmax_scale: float = 0.0, max_cands=None):
+                 softmax_scale: float = 0.0, max_cands=None, row_offsets=None):
         self.sb = sb
         self.device = device
         self.ragged = sb.ragged if ragged is None else bool(ragged)
@@ -47,9 +49,12 @@ class DeviceStage:
         # The mutual-scoring stage reduces every key by the mean over its anchor rows.
         rr = occam.ROWS_MEAN if sb.stage == "mut" else occam.ROWS_MAX
         if self.ragged:
-            self.q_off = _i32(sb.q_off, device)
+            if row_offsets is False and np.any(sb.T != sb.T[0]):
+                raise ValueError("row_offsets=False needs the same row count in every sample")
+            self.q_off = None if row_offsets is False else _i32(sb.q_off, device)
             self.k_off = _i32(sb.k_off, device)
-            self.problem = occam.Problem(sb.B, sb.H, sb.Hkv, sb.d, sb.R, q_offsets=self.q_off,
+            self.problem = occam.Problem(sb.B, sb.H, sb.Hkv, sb.d, sb.R, rows=int(sb.T[0]),
+                                         q_offsets=self.q_off,
                                          key_offsets=self.k_off, max_rows=int(sb.T.max()),
                                          max_cands=int(sb.N.max()) if max_cands is None
                                          else int(max_cands), dtype=sb.dtype,

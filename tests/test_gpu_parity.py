@@ -20,11 +20,12 @@ from parity import (RTOL, check_bookkeeping, check_rows, check_scores, check_sel
 pytestmark = pytest.mark.gpu
 
 
-def run_and_check(sb, lam, reduce=oracle.REG_MEAN, ragged=None, rows=True, max_cands=None):
+def run_and_check(sb, lam, reduce=oracle.REG_MEAN, ragged=None, rows=True, max_cands=None,
+                  row_offsets=None):
     print("case: %s/%s B=%d R=%d H=%d Hkv=%d d=%d T=%s N=%s dtype=%s lam=%.6g ragged=%s" % (
         sb.workload, sb.stage, sb.B, sb.R, sb.H, sb.Hkv, sb.d, sb.T[:4], sb.N[:4], sb.dtype, lam,
         ragged), flush=True)
-    ds = DeviceStage(sb, ragged=ragged, max_cands=max_cands)
+    ds = DeviceStage(sb, ragged=ragged, max_cands=max_cands, row_offsets=row_offsets)
     ds.prune(lam, reduce=reduce, with_rows=rows)
     g = ds.host(with_rows=rows)
     o = oracle_prune(sb, lam, reduce=reduce)
@@ -193,6 +194,15 @@ def test_lambda_zero_keeps_everything_and_huge_keeps_nothing():
     assert np.array_equal(g["kept_count"], sb.N)
     g, _ = run_and_check(sb, 1e30)
     assert np.all(g["kept_count"] == 0) and np.all(g["kept_offsets"] == 0)
+
+
+def test_uniform_rows_with_ragged_keys():
+    # Ragged key counts, every sample 128 or 256 text rows, passed without row offsets:
+    # the scoring pass's full-row-block form meets the ragged task mapping (and, at 256
+    # rows, the combine over two row blocks).
+    for T in (128, 256):
+        sb = custom_stage(B=4, R=4, H=8, Hkv=8, d=128, T=[T] * 4, N=[700, 30, 0, 260], seed=T)
+        run_and_check(sb, 1.0, ragged=True, row_offsets=False)
 
 
 def test_ragged_text_with_many_samples():
