@@ -127,6 +127,9 @@ typedef struct {
     float softmax_scale;    /* 0 => 1/sqrt(d), the scale of Eq. (1)                  */
     int32_t visual_row_reduce; /* occam_row_reduce; 0 (MAX) when zero-initialised    */
 } occam_problem;
+/* The two offset arrays are independent: ragged key counts with the same row count in
+ * every sample (q_offsets NULL, key_offsets set) is a valid problem, and with T a
+ * multiple of 128 it lets the text-row scoring use its full-row-block form. */
 
 /* One row tensor gathered with the survivors (occam_gather / occam_prune).
  * The source row of visual token v of sample b is
