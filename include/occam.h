@@ -47,15 +47,19 @@
  *
  * Ownership.  Every pointer argument is DEVICE memory owned by the caller,
  * except `const occam_problem *` and `const occam_rows *`, which are host
- * structs read during the call only.  The library allocates no memory and
- * keeps no mutable global state; calls on different streams may overlap when
- * their output and workspace buffers are distinct.
+ * structs read during the call only.  The library allocates no memory; calls on
+ * different streams may overlap when their output and workspace buffers are
+ * distinct; it keeps no mutable global state.
  *
- * Errors.  Arguments are validated on the host before anything is enqueued;
- * on any error nothing is launched and the outputs are untouched.  Calls are
+ * Errors.  Arguments are validated on the host before anything is enqueued:
+ * OCCAM_ERR_INVALID_ARG, OCCAM_ERR_UNSUPPORTED and OCCAM_ERR_WORKSPACE mean
+ * nothing was launched and the outputs are untouched.  OCCAM_ERR_HIP means the
+ * HIP runtime rejected a launch; kernels of the same call enqueued before it
+ * may already run, so the outputs are then undefined.  Calls are
  * asynchronous: kernel faults surface at the caller's next synchronisation of
  * `stream`.  Inputs must be finite.  Device-side offsets must be
  * non-decreasing with 1 <= T_b <= max_rows and 0 <= N_b <= max_cands.
+ * Batches are limited to B <= 65535 (OCCAM_ERR_UNSUPPORTED beyond).
  *
  * Precision.  Logits and probabilities are computed in float32 from float32
  * or bfloat16 inputs; bfloat16 products are exact in float32.

@@ -349,14 +349,14 @@ static hipError_t cls_stream_launch(const Prob& p, const void* q, const void* k,
     const int nc = p.d * (BF16 ? 2 : 4) / 16;
     const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
     dim3 grid(nchunks, p.B);
+    const dim3 blk(kClsThreads);
     switch (NC * p.Hkv / 64) {
-    case 1: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 1>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks, nc); break;
-    case 2: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 2>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks, nc); break;
-    case 3: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 3>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks, nc); break;
-    case 4: hipLaunchKernelGGL((cls_stream_kernel<BF16, NC, 4>), grid, dim3(kClsThreads), 0, s, p, q, k, logits, stats, kpw, nchunks, nc); break;
+    case 1: return launch(cls_stream_kernel<BF16, NC, 1>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc);
+    case 2: return launch(cls_stream_kernel<BF16, NC, 2>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc);
+    case 3: return launch(cls_stream_kernel<BF16, NC, 3>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc);
+    case 4: return launch(cls_stream_kernel<BF16, NC, 4>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc);
     default: return hipErrorInvalidValue;
     }
-    return hipGetLastError();
 }
 
 template <bool BF16>
@@ -384,12 +384,10 @@ hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void*
     dim3 grid(nchunks, p.B);
     const size_t smem = cls_logits_smem(p, bf16, kpw);
     if (bf16)
-        hipLaunchKernelGGL(cls_logits_kernel<true>, grid, dim3(kClsThreads), smem, s, p, q, k,
-                           logits, stats, kpw, nchunks);
-    else
-        hipLaunchKernelGGL(cls_logits_kernel<false>, grid, dim3(kClsThreads), smem, s, p, q, k,
-                           logits, stats, kpw, nchunks);
-    return hipGetLastError();
+        return launch(cls_logits_kernel<true>, grid, dim3(kClsThreads), smem, s, p, q, k, logits,
+                      stats, kpw, nchunks);
+    return launch(cls_logits_kernel<false>, grid, dim3(kClsThreads), smem, s, p, q, k, logits,
+                  stats, kpw, nchunks);
 }
 
 hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const float2* stats,
@@ -398,12 +396,10 @@ hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const
     const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
     dim3 grid(nchunks, p.B);
     if (bf16)
-        hipLaunchKernelGGL(cls_scores_kernel<true>, grid, dim3(kClsThreads), 0, s, p, logits, stats,
-                           row_lse, scores, kpw, nchunks);
-    else
-        hipLaunchKernelGGL(cls_scores_kernel<false>, grid, dim3(kClsThreads), 0, s, p, logits,
-                           stats, row_lse, scores, kpw, nchunks);
-    return hipGetLastError();
+        return launch(cls_scores_kernel<true>, grid, dim3(kClsThreads), 0, s, p, logits, stats,
+                      row_lse, scores, kpw, nchunks);
+    return launch(cls_scores_kernel<false>, grid, dim3(kClsThreads), 0, s, p, logits, stats,
+                  row_lse, scores, kpw, nchunks);
 }
 
 }  // namespace occam

@@ -721,15 +721,15 @@ template <int DS, bool HALF, bool COLSUM, int RG>
 static hipError_t stats_launch_rg(const Prob& p, const void* q, const void* k, float* lse2,
                                   const float* lse_in, int lse_natural, float* part, hipStream_t s) {
     const size_t smem = text_stats_smem(DS * 16, RG);
-    static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&text_stats_kernel<DS, HALF, COLSUM, RG>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kScoreSmemMax);
+    static std::atomic<uint64_t> lds_set{0};
+    const hipError_t attr = allow_lds(
+        reinterpret_cast<const void*>(&text_stats_kernel<DS, HALF, COLSUM, RG>), (int)kScoreSmemMax,
+        lds_set);
     if (attr != hipSuccess) return attr;
     dim3 grid((p.max_rows + kTxtRows - 1) / kTxtRows * p.H * p.B);
-    hipLaunchKernelGGL((text_stats_kernel<DS, HALF, COLSUM, RG>), grid, dim3(kStatsThreads), smem,
-                       s, p, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse2,
-                       lse_in, lse_natural, part);
-    return hipGetLastError();
+    return launch(text_stats_kernel<DS, HALF, COLSUM, RG>, grid, dim3(kStatsThreads), smem, s, p,
+                  static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse2, lse_in,
+                  lse_natural, part);
 }
 
 // Four waves of 32 rows on one key stream.  Two streams of two 64-row waves reuse each
@@ -783,17 +783,18 @@ template <int DS, bool HALF, bool FULL>
 static hipError_t score_launch(const Prob& p, const void* q, const void* k, const float* lse,
                                int lse_natural, float* scores, float* part, hipStream_t s) {
     const size_t smem = text_score_smem(p.H, DS * 16);
-    // The tile needs more than the default 64 KB of dynamic LDS: raise the limit once.
-    static const hipError_t attr = hipFuncSetAttribute(
-        reinterpret_cast<const void*>(&text_score_kernel<DS, HALF, FULL>),
-        hipFuncAttributeMaxDynamicSharedMemorySize, (int)kScoreSmemMax);
+    // The tile needs more than the default 64 KB of dynamic LDS: raise the limit (once per
+    // device).
+    static std::atomic<uint64_t> lds_set{0};
+    const hipError_t attr = allow_lds(
+        reinterpret_cast<const void*>(&text_score_kernel<DS, HALF, FULL>), (int)kScoreSmemMax,
+        lds_set);
     if (attr != hipSuccess) return attr;
     const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
     dim3 grid((p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg * nrb * p.B);
-    hipLaunchKernelGGL((text_score_kernel<DS, HALF, FULL>), grid, dim3(kScoreThreads), smem, s, p,
-                       static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
-                       lse_natural, scores, nrb > 1 ? part : nullptr);
-    return hipGetLastError();
+    return launch(text_score_kernel<DS, HALF, FULL>, grid, dim3(kScoreThreads), smem, s, p,
+                  static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
+                  lse_natural, scores, nrb > 1 ? part : nullptr);
 }
 
 template <int DS, bool HALF>
@@ -807,8 +808,7 @@ static hipError_t score_ds(const Prob& p, const void* q, const void* k, const fl
     const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
     if (nrb == 1) return hipSuccess;
     dim3 cgrid((p.R + p.max_cands + 255) / 256, p.B);
-    hipLaunchKernelGGL(text_rows_combine_kernel, cgrid, dim3(256), 0, s, p, part, scores);
-    return hipGetLastError();
+    return launch(text_rows_combine_kernel, cgrid, dim3(256), 0, s, p, part, scores);
 }
 
 // d = 16*DS (HALF = false) or 16*DS - 8 (HALF = true), d <= 128.
@@ -845,8 +845,7 @@ hipError_t launch_text_colsum(const Prob& p, const void* q, const void* k, const
     const hipError_t e = colsum_any(p, q, k, lse, lse_natural, part, s);
     if (e != hipSuccess) return e;
     dim3 grid((p.R + p.max_cands + 255) / 256, p.B);
-    hipLaunchKernelGGL(text_colsum_reduce_kernel, grid, dim3(256), 0, s, p, part, scores);
-    return hipGetLastError();
+    return launch(text_colsum_reduce_kernel, grid, dim3(256), 0, s, p, part, scores);
 }
 
 }  // namespace occam

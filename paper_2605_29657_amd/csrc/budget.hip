@@ -202,15 +202,17 @@ hipError_t launch_match_lambda(const Prob& p, const float* scores, int reduce, f
     const int chunks = (p.max_cands + kMatchChunk - 1) / kMatchChunk;
     const dim3 grid(p.B, chunks > 0 ? chunks : 1);
     const dim3 block(kMatchThreads);
-    hipLaunchKernelGGL(match_init_kernel, dim3(1), block, 0, s, p, k_target, st);
+    hipError_t e = launch(match_init_kernel, dim3(1), block, 0, s, p, k_target, st);
+    if (e != hipSuccess) return e;
     if (chunks > 0) {
-        hipLaunchKernelGGL(match_hist_kernel<0>, grid, block, 0, s, p, scores, reduce, st);
-        hipLaunchKernelGGL(match_hist_kernel<1>, grid, block, 0, s, p, scores, reduce, st);
-        hipLaunchKernelGGL(match_hist_kernel<2>, grid, block, 0, s, p, scores, reduce, st);
-        hipLaunchKernelGGL(match_hist_kernel<3>, grid, block, 0, s, p, scores, reduce, st);
+        if ((e = launch(match_hist_kernel<0>, grid, block, 0, s, p, scores, reduce, st)) != hipSuccess ||
+            (e = launch(match_hist_kernel<1>, grid, block, 0, s, p, scores, reduce, st)) != hipSuccess ||
+            (e = launch(match_hist_kernel<2>, grid, block, 0, s, p, scores, reduce, st)) != hipSuccess ||
+            (e = launch(match_hist_kernel<3>, grid, block, 0, s, p, scores, reduce, st)) != hipSuccess)
+            return e;
     }
-    hipLaunchKernelGGL(match_count_kernel, grid, block, 0, s, p, scores, reduce, k_target, st, lambda, mean_kept);
-    return hipGetLastError();
+    return launch(match_count_kernel, grid, block, 0, s, p, scores, reduce, k_target, st, lambda,
+                  mean_kept);
 }
 
 }  // namespace occam

@@ -5,6 +5,7 @@
 #include <stdint.h>
 #include <string.h>
 
+
 #include "occam.h"
 #include "occam_internal.hpp"
 
@@ -47,6 +48,8 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
     const long long keys_cap = (long long)B * (R + (long long)max_cands);
     const long long rows_cap = (long long)B * max_rows;
     if (keys_cap * H >= (1LL << 31) || rows_cap * H >= (1LL << 31)) return OCCAM_ERR_UNSUPPORTED;
+    // Several kernels put the sample index in grid.y, whose extent is at most 65535.
+    if (B > kMaxGridY) return OCCAM_ERR_UNSUPPORTED;
     if (d % (bf16 ? 8 : 4) != 0) return OCCAM_ERR_UNSUPPORTED;
 
     Plan P;
@@ -178,7 +181,8 @@ occam_status key_layout(const occam_problem* pr, Prob* out, int* bf16) {
     const int max_cands = x.key_offsets ? x.max_cands : x.cands;
     if (max_cands < 0) return OCCAM_ERR_INVALID_ARG;
     if (x.key_offsets && !aligned(x.key_offsets, 4)) return OCCAM_ERR_INVALID_ARG;
-    if ((long long)x.batch * (x.num_registers + (long long)max_cands) >= (1LL << 31))
+    if ((long long)x.batch * (x.num_registers + (long long)max_cands) >= (1LL << 31) ||
+        x.batch > kMaxGridY)
         return OCCAM_ERR_UNSUPPORTED;
     Prob p;
     memset(&p, 0, sizeof p);
@@ -187,6 +191,41 @@ occam_status key_layout(const occam_problem* pr, Prob* out, int* bf16) {
     *out = p;
     *bf16 = x.dtype == OCCAM_BF16;
     return OCCAM_OK;
+}
+
+// Argument checks of occam_prune (and its allocation-free variant) before any HIP call.
+occam_status prune_args(const occam_problem* problem, const void* q, const void* k,
+                        const float* row_lse, float lambda, int32_t reduce,
+                        const int32_t* index_map, int32_t n, const occam_rows* tensors,
+                        const float* scores, const float* tau, const int32_t* kept_idx,
+                        const int32_t* kept_count, const int32_t* kept_offsets, Plan* P,
+                        RowTensors* rows) {
+    occam_status st = make_plan(problem, P);
+    if (st != OCCAM_OK) return st;
+    if (!q || !k || !kept_idx || !kept_count || !kept_offsets || !aligned(q, 16) ||
+        !aligned(k, 16) || !aligned(kept_idx, 4) || !aligned(kept_count, 4) ||
+        !aligned(kept_offsets, 4) || (scores && !aligned(scores, 4)) || (tau && !aligned(tau, 4)) ||
+        (row_lse && !aligned(row_lse, 4)) || (index_map && !aligned(index_map, 4)) ||
+        !lambda_ok(lambda) || !reduce_ok(reduce))
+        return OCCAM_ERR_INVALID_ARG;
+    return rows_from(n, tensors, rows);
+}
+
+// Steps 1-5 on a validated plan and a workspace of at least P.total bytes.
+occam_status run_prune(const Plan& P, const void* q, const void* k, const float* row_lse,
+                       float lambda, int32_t reduce, const int32_t* index_map,
+                       const RowTensors& rows, float* scores, float* tau, int32_t* kept_idx,
+                       int32_t* kept_count, int32_t* kept_offsets, void* workspace,
+                       hipStream_t stream) {
+    occam_status st;
+    float* sc = scores ? scores : ws_at<float>(workspace, P.off_scores);
+    float* tu = tau ? tau : ws_at<float>(workspace, P.off_tau);
+    int* slot = ws_at<int>(workspace, P.off_slot);
+    if ((st = run_score(P, q, k, row_lse, sc, workspace, stream)) != OCCAM_OK) return st;
+    st = hip_ok(launch_select(P.p, sc, nullptr, 1, lambda, reduce, tu, slot, kept_count, stream));
+    if (st != OCCAM_OK) return st;
+    return hip_ok(launch_pack_gather(P.p, slot, kept_count, index_map, kept_idx, kept_offsets,
+                                     nullptr, nullptr, rows, stream));
 }
 
 }  // namespace
@@ -300,25 +339,13 @@ occam_status occam_prune(const occam_problem* problem, const void* q, const void
                          int32_t* kept_offsets, void* workspace, size_t ws_bytes,
                          hipStream_t stream) {
     Plan P;
-    occam_status st = make_plan(problem, &P);
-    if (st != OCCAM_OK) return st;
-    if (!q || !k || !kept_idx || !kept_count || !kept_offsets || !aligned(q, 16) ||
-        !aligned(k, 16) || !aligned(kept_idx, 4) || !aligned(kept_count, 4) ||
-        !aligned(kept_offsets, 4) || (scores && !aligned(scores, 4)) || (tau && !aligned(tau, 4)) ||
-        (row_lse && !aligned(row_lse, 4)) || (index_map && !aligned(index_map, 4)) ||
-        !lambda_ok(lambda) || !reduce_ok(reduce))
-        return OCCAM_ERR_INVALID_ARG;
     RowTensors rows;
-    if ((st = rows_from(n, tensors, &rows)) != OCCAM_OK) return st;
-    if ((st = check_ws(P, workspace, ws_bytes)) != OCCAM_OK) return st;
-    float* sc = scores ? scores : ws_at<float>(workspace, P.off_scores);
-    float* tu = tau ? tau : ws_at<float>(workspace, P.off_tau);
-    int* slot = ws_at<int>(workspace, P.off_slot);
-    if ((st = run_score(P, q, k, row_lse, sc, workspace, stream)) != OCCAM_OK) return st;
-    st = hip_ok(launch_select(P.p, sc, nullptr, 1, lambda, reduce, tu, slot, kept_count, stream));
+    occam_status st = prune_args(problem, q, k, row_lse, lambda, reduce, index_map, n, tensors,
+                                 scores, tau, kept_idx, kept_count, kept_offsets, &P, &rows);
     if (st != OCCAM_OK) return st;
-    return hip_ok(launch_pack_gather(P.p, slot, kept_count, index_map, kept_idx, kept_offsets,
-                                     nullptr, nullptr, rows, stream));
+    if ((st = check_ws(P, workspace, ws_bytes)) != OCCAM_OK) return st;
+    return run_prune(P, q, k, row_lse, lambda, reduce, index_map, rows, scores, tau, kept_idx,
+                     kept_count, kept_offsets, workspace, stream);
 }
 
 occam_status occam_match_lambda(const occam_problem* problem, const float* scores, int32_t reduce,

@@ -5,9 +5,46 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <atomic>
+#include <tuple>
+#include <utility>
+
 namespace occam {
 
+// Launch `kernel` and return the status of this launch alone (hipLaunchKernel reports
+// its own result; hipGetLastError would also report an unrelated earlier failure).
+// The arguments are converted to the kernel's parameter types before their addresses
+// are taken.
+template <typename... KArgs, typename... Args>
+inline hipError_t launch(void (*kernel)(KArgs...), dim3 grid, dim3 block, size_t smem,
+                         hipStream_t s, Args&&... args) {
+    static_assert(sizeof...(KArgs) == sizeof...(Args), "kernel argument count");
+    std::tuple<KArgs...> vals(std::forward<Args>(args)...);
+    return std::apply(
+        [&](auto&... v) {
+            void* ptrs[] = {static_cast<void*>(&v)...};
+            return hipLaunchKernel(reinterpret_cast<const void*>(kernel), grid, block, ptrs,
+                                   smem, s);
+        },
+        vals);
+}
+
+// Raise the dynamic LDS limit of `kernel` to `bytes` on the current device, once per
+// device: `done` holds one bit per device ordinal (0..63) whose call succeeded.  A
+// failure is returned and the call is tried again next time.
+inline hipError_t allow_lds(const void* kernel, int bytes, std::atomic<uint64_t>& done) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const uint64_t bit = (dev >= 0 && dev < 64) ? (uint64_t(1) << dev) : 0;
+    if (bit && (done.load(std::memory_order_acquire) & bit)) return hipSuccess;
+    e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e == hipSuccess && bit) done.fetch_or(bit, std::memory_order_acq_rel);
+    return e;
+}
+
 constexpr int kWave = 64;
+constexpr int kMaxGridY = 65535;   // launch limit of grid.y (the sample index of several kernels)
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr float kLog2e = 1.4426950408889634f;
@@ -194,7 +231,7 @@ inline int cls_keys_per_wg(int H, int Hkv, int d, int elem_bytes) {
 }
 
 // ---------------------------------------------------------------------------
-// Launchers (defined in the .hip files).  All return hipGetLastError().
+// Launchers (defined in the .hip files).  Each returns the status of its own launches.
 hipError_t launch_select_topk(const Prob& p, const float* scores, int k_keep, int* slot,
                               int* count, hipStream_t s);
 // Selection state of budget matching, in the workspace.

@@ -60,12 +60,10 @@ hipError_t launch_register_redirect(const Prob& p, int bf16, void* h, int width,
     if (n_channels == 0) return hipSuccess;
     dim3 grid(p.B, (n_channels + 3) / 4);
     if (bf16)
-        hipLaunchKernelGGL(register_redirect_kernel<true>, grid, dim3(256), 0, s, p,
-                           static_cast<char*>(h), width, stride, channels, n_channels, reg_slot);
-    else
-        hipLaunchKernelGGL(register_redirect_kernel<false>, grid, dim3(256), 0, s, p,
-                           static_cast<char*>(h), width, stride, channels, n_channels, reg_slot);
-    return hipGetLastError();
+        return launch(register_redirect_kernel<true>, grid, dim3(256), 0, s, p,
+                      static_cast<char*>(h), width, stride, channels, n_channels, reg_slot);
+    return launch(register_redirect_kernel<false>, grid, dim3(256), 0, s, p, static_cast<char*>(h),
+                  width, stride, channels, n_channels, reg_slot);
 }
 
 }  // namespace occam

@@ -168,21 +168,18 @@ hipError_t launch_threshold(const Prob& p, const float* scores, float lambda, in
                             float* tau, hipStream_t s)
 {
     if (reduce == kRefCandMean)
-        hipLaunchKernelGGL(threshold_mean_kernel, dim3(p.B), dim3(kSelThreads), 0, s, p, scores,
-                           lambda, tau);
-    else
-        hipLaunchKernelGGL(threshold_kernel, dim3((p.B + 255) / 256), dim3(256), 0, s, p, scores,
-                           lambda, reduce, tau);
-    return hipGetLastError();
+        return launch(threshold_mean_kernel, dim3(p.B), dim3(kSelThreads), 0, s, p, scores, lambda,
+                      tau);
+    return launch(threshold_kernel, dim3((p.B + 255) / 256), dim3(256), 0, s, p, scores, lambda,
+                  reduce, tau);
 }
 
 hipError_t launch_select(const Prob& p, const float* scores, const float* tau, int fuse_tau,
                          float lambda, int reduce, float* tau_out, int* slot, int* count,
                          hipStream_t s)
 {
-    hipLaunchKernelGGL(select_kernel, dim3(p.B), dim3(kSelectThreads), 0, s, p, scores, tau, fuse_tau,
-                       lambda, reduce, tau_out, slot, count);
-    return hipGetLastError();
+    return launch(select_kernel, dim3(p.B), dim3(kSelectThreads), 0, s, p, scores, tau, fuse_tau,
+                  lambda, reduce, tau_out, slot, count);
 }
 
 hipError_t launch_pack_gather(const Prob& p, const int* slot, const int* count,
@@ -199,10 +196,8 @@ hipError_t launch_pack_gather(const Prob& p, const int* slot, const int* count,
     long long cap = (4096 + p.B - 1) / p.B;
     long long G = per < cap ? per : cap;
     if (G < 1) G = 1;
-    hipLaunchKernelGGL(pack_gather_kernel, dim3((unsigned)G, p.B), dim3(kGatherThreads), 0, s, p,
-                       slot, count, index_map, kept_idx, kept_offsets, packed_idx, packed_offsets,
-                       rows);
-    return hipGetLastError();
+    return launch(pack_gather_kernel, dim3((unsigned)G, p.B), dim3(kGatherThreads), 0, s, p, slot,
+                  count, index_map, kept_idx, kept_offsets, packed_idx, packed_offsets, rows);
 }
 
 }  // namespace occam

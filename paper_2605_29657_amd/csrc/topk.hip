@@ -112,9 +112,8 @@ __global__ __launch_bounds__(kSelThreads) void select_topk_kernel(
 hipError_t launch_select_topk(const Prob& p, const float* scores, int k_keep, int* slot,
                               int* count, hipStream_t s)
 {
-    hipLaunchKernelGGL(select_topk_kernel, dim3(p.B), dim3(kSelThreads), 0, s, p, scores, k_keep,
-                       slot, count);
-    return hipGetLastError();
+    return launch(select_topk_kernel, dim3(p.B), dim3(kSelThreads), 0, s, p, scores, k_keep, slot,
+                  count);
 }
 
 }  // namespace occam

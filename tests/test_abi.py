@@ -249,3 +249,12 @@ def test_mean_threshold_is_an_accepted_reduction(L):
     p = good_problem()
     assert L.occam_threshold(p.ref, None, ctypes.c_float(1.0), occam.REF_CAND_MEAN, FAKE, None) == \
         occam.ERR_INVALID_ARG
+
+
+def test_unsupported_batch_beyond_the_grid_limit(L):
+    # The sample index sits in grid.y of several kernels (at most 65535).
+    p = good_problem(batch=65536, cands=4)
+    assert ws_size(p) == 0
+    assert L.occam_score(p.ref, FAKE, FAKE, None, FAKE, FAKE, 1 << 40, None) == occam.ERR_UNSUPPORTED
+    assert ws_size(good_problem(batch=65535, cands=4)) > 0
+
