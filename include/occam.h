@@ -49,7 +49,9 @@
  * except `const occam_problem *` and `const occam_rows *`, which are host
  * structs read during the call only.  The library allocates no memory; calls on
  * different streams may overlap when their output and workspace buffers are
- * distinct; it keeps no mutable global state.
+ * distinct.  Its only global state is the built-in workspace of
+ * occam_prune_noalloc (one static device array per GPU) and the per-device
+ * addresses of that array, looked up once.
  *
  * Errors.  Arguments are validated on the host before anything is enqueued:
  * OCCAM_ERR_INVALID_ARG, OCCAM_ERR_UNSUPPORTED and OCCAM_ERR_WORKSPACE mean
@@ -222,6 +224,26 @@ occam_status occam_prune(const occam_problem *problem, const void *q, const void
                          float *scores, float *tau, int32_t *kept_idx, int32_t *kept_count,
                          int32_t *kept_offsets, void *workspace, size_t ws_bytes,
                          hipStream_t stream);
+
+/* occam_prune without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops, harnesses that
+ * forbid hipMalloc).  It runs exactly the kernels of occam_prune, with the
+ * workspace taken from a static device array built into the library: 32 MiB per
+ * GPU, held from the library's first use on that GPU until the process ends.
+ * A problem whose occam_workspace_size exceeds 32 MiB returns
+ * OCCAM_ERR_WORKSPACE (use occam_prune with a workspace of its own).  The
+ * array's device address is looked up once per device, on the first call whose
+ * stream belongs to that device (OCCAM_ERR_HIP if the lookup fails).  The call
+ * allocates nothing.  Every call on one GPU shares that GPU's array, so calls
+ * that overlap on one GPU (different streams, or different host threads)
+ * race; calls ordered on one stream do not.  The array needs no clearing: every
+ * call writes what it reads. */
+occam_status occam_prune_noalloc(const occam_problem *problem, const void *q, const void *k,
+                                 const float *row_lse, float lambda, int32_t reduce,
+                                 const int32_t *index_map, int32_t n,
+                                 const occam_rows *tensors, float *scores, float *tau,
+                                 int32_t *kept_idx, int32_t *kept_count, int32_t *kept_offsets,
+                                 hipStream_t stream);
 
 /* Budget matching (Appendix Eq. lambda2_budget_matching_appendix) over the batch
  * as the calibration set: the mean kept count (1/B) sum_b |{v : s_b(v) >= lambda *

@@ -5,6 +5,8 @@
 #include <stdint.h>
 #include <string.h>
 
+#include <atomic>
+#include <mutex>
 
 #include "occam.h"
 #include "occam_internal.hpp"
@@ -228,6 +230,39 @@ occam_status run_prune(const Plan& P, const void* q, const void* k, const float*
                                      nullptr, nullptr, rows, stream));
 }
 
+// ---------------------------------------------------------------------------
+// Built-in workspace of occam_prune_noalloc, for callers that cannot allocate device
+// memory.  The loader gives every GPU that runs this library its own copy of the array
+// (held until the process ends).  In host code `scratch` names a host-side stand-in, not
+// device memory: only the address that hipGetSymbolAddress returns for the device,
+// looked up once per device and kept in scratch_ptr, is ever handed to a kernel.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+std::atomic<void*> scratch_ptr[kMaxDevices];
+
+// The device address of `scratch` on the device that `stream` belongs to, or null.
+void* scratch_for(hipStream_t stream) {
+    int dev = -1;
+    if (hipStreamGetDevice(stream, &dev) != hipSuccess || dev < 0 || dev >= kMaxDevices)
+        return nullptr;
+    void* ptr = scratch_ptr[dev].load(std::memory_order_acquire);
+    if (ptr) return ptr;
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    ptr = scratch_ptr[dev].load(std::memory_order_acquire);
+    if (ptr) return ptr;
+    int cur = -1;
+    if (hipGetDevice(&cur) != hipSuccess) return nullptr;
+    if (cur != dev && hipSetDevice(dev) != hipSuccess) return nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (cur != dev) (void)hipSetDevice(cur);
+    if (e != hipSuccess || !ptr || !aligned(ptr, kAlign)) return nullptr;
+    scratch_ptr[dev].store(ptr, std::memory_order_release);
+    return ptr;
+}
+
 }  // namespace
 
 extern "C" {
@@ -346,6 +381,24 @@ occam_status occam_prune(const occam_problem* problem, const void* q, const void
     if ((st = check_ws(P, workspace, ws_bytes)) != OCCAM_OK) return st;
     return run_prune(P, q, k, row_lse, lambda, reduce, index_map, rows, scores, tau, kept_idx,
                      kept_count, kept_offsets, workspace, stream);
+}
+
+occam_status occam_prune_noalloc(const occam_problem* problem, const void* q, const void* k,
+                                 const float* row_lse, float lambda, int32_t reduce,
+                                 const int32_t* index_map, int32_t n,
+                                 const occam_rows* tensors, float* scores, float* tau,
+                                 int32_t* kept_idx, int32_t* kept_count, int32_t* kept_offsets,
+                                 hipStream_t stream) {
+    Plan P;
+    RowTensors rows;
+    occam_status st = prune_args(problem, q, k, row_lse, lambda, reduce, index_map, n, tensors,
+                                 scores, tau, kept_idx, kept_count, kept_offsets, &P, &rows);
+    if (st != OCCAM_OK) return st;
+    if (P.total > kScratchBytes) return OCCAM_ERR_WORKSPACE;
+    void* ws = scratch_for(stream);
+    if (!ws) return OCCAM_ERR_HIP;
+    return run_prune(P, q, k, row_lse, lambda, reduce, index_map, rows, scores, tau, kept_idx,
+                     kept_count, kept_offsets, ws, stream);
 }
 
 occam_status occam_match_lambda(const occam_problem* problem, const float* scores, int32_t reduce,

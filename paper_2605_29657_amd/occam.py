@@ -28,7 +28,8 @@ MAX_ROW_TENSORS = 8
 
 EXPORTS = ("occam_status_string", "occam_version", "occam_workspace_size", "occam_score",
            "occam_threshold", "occam_select", "occam_gather", "occam_prune",
-           "occam_register_redirect", "occam_match_lambda", "occam_select_topk")
+           "occam_register_redirect", "occam_match_lambda", "occam_select_topk",
+           "occam_prune_noalloc")
 
 
 class OccamError(RuntimeError):
@@ -86,6 +87,9 @@ def lib():
         L.occam_prune.argtypes = [P, vp, vp, vp, f32, i32, vp, i32, RP, vp, vp, vp, vp, vp, vp,
                                   sz, vp]
         L.occam_prune.restype = i32
+        L.occam_prune_noalloc.argtypes = [P, vp, vp, vp, f32, i32, vp, i32, RP, vp, vp, vp, vp,
+                                          vp, vp]
+        L.occam_prune_noalloc.restype = i32
         L.occam_register_redirect.argtypes = [P, vp, i32, ctypes.c_int64, vp, i32, i32, vp]
         L.occam_register_redirect.restype = i32
         L.occam_match_lambda.argtypes = [P, vp, i32, f32, vp, vp, vp, sz, vp]
@@ -209,6 +213,16 @@ def prune(problem, q, k, lam, kept_idx, kept_count, kept_offsets, ws, reduce=REG
                              _ptr(index_map), n, arr, _ptr(scores), _ptr(tau), _ptr(kept_idx),
                              _ptr(kept_count), _ptr(kept_offsets), _ptr(ws),
                              0 if ws is None else ws.numel(), _stream(stream)))
+
+
+def prune_noalloc(problem, q, k, lam, kept_idx, kept_count, kept_offsets, reduce=REG_MEAN,
+                  rows=None, scores=None, tau=None, row_lse=None, index_map=None, stream=None):
+    """occam_prune_noalloc: occam_prune on the library's built-in workspace."""
+    n, arr = _rows_array(rows)
+    _check(lib().occam_prune_noalloc(problem.ref, _ptr(q), _ptr(k), _ptr(row_lse), float(lam),
+                                     int(reduce), _ptr(index_map), n, arr, _ptr(scores),
+                                     _ptr(tau), _ptr(kept_idx), _ptr(kept_count),
+                                     _ptr(kept_offsets), _stream(stream)))
 
 
 def match_lambda(problem, scores, k_target, lam_out, ws, mean_kept=None, reduce=REG_MEAN,

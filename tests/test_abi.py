@@ -258,3 +258,25 @@ def test_unsupported_batch_beyond_the_grid_limit(L):
     assert L.occam_score(p.ref, FAKE, FAKE, None, FAKE, FAKE, 1 << 40, None) == occam.ERR_UNSUPPORTED
     assert ws_size(good_problem(batch=65535, cands=4)) > 0
 
+
+def test_prune_noalloc_validation(L):
+    # Checks run before any HIP call, as in occam_prune; none of these reach a launch.
+    p = good_problem()
+    args = lambda **kw: dict(dict(q=FAKE, k=FAKE, lam=1.0, idx=FAKE, cnt=FAKE, off=FAKE), **kw)
+
+    def call(prob, a):
+        return L.occam_prune_noalloc(prob.ref, a["q"], a["k"], None, a["lam"], 0, None, 0, None,
+                                     None, None, a["idx"], a["cnt"], a["off"], None)
+
+    assert call(p, args(q=None)) == occam.ERR_INVALID_ARG
+    assert call(p, args(k=FAKE + 8)) == occam.ERR_INVALID_ARG
+    assert call(p, args(lam=-1.0)) == occam.ERR_INVALID_ARG
+    assert call(p, args(off=None)) == occam.ERR_INVALID_ARG
+    assert call(good_problem(batch=0), args()) == occam.ERR_INVALID_ARG
+    assert call(good_problem(head_dim=6), args()) == occam.ERR_UNSUPPORTED
+    # A problem whose workspace exceeds the built-in 32 MiB is refused, not truncated.
+    big = good_problem(batch=1024, cands=4096)
+    assert ws_size(big) > (32 << 20)
+    assert call(big, args()) == occam.ERR_WORKSPACE
+    assert L.occam_prune_noalloc(None, FAKE, FAKE, None, 1.0, 0, None, 0, None, None, None, FAKE,
+                                 FAKE, FAKE, None) == occam.ERR_INVALID_ARG
