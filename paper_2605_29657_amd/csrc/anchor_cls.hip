@@ -33,11 +33,12 @@ __device__ __forceinline__ float cls_exp(float x) {
 template <bool BF16>
 __global__ __launch_bounds__(kClsThreads) void cls_logits_kernel(
     Prob p, const void* __restrict__ qv, const void* __restrict__ kv,
-    float* __restrict__ logits, float2* __restrict__ stats, int kpw, int nchunks)
+    float* __restrict__ logits, float2* __restrict__ stats, int kpw, int nchunks, Finish fin)
 {
     extern __shared__ float smem[];
     constexpr int CE = BF16 ? 8 : 4;            // elements per 16-byte chunk
     const int c = blockIdx.x, b = blockIdx.y;
+    if (c == 0 && b == 0) clear_done(fin, p.B);  // counters of the cls_scores launch
     const int S = keys_of(p, b);
     const int s0 = c * kpw;
     if (s0 >= S) return;                        // uniform over the workgroup
@@ -75,7 +76,7 @@ __global__ __launch_bounds__(kClsThreads) void cls_logits_kernel(
         for (int ci = lane; ci < CPK; ci += kWave) {
             const u32x4 w = __builtin_nontemporal_load(krow + ci);
             float kf[CE];
-            if (BF16) {
+            if constexpr (BF16) {
                 kf[0] = bf16_lo(w.x); kf[1] = bf16_hi(w.x);
                 kf[2] = bf16_lo(w.y); kf[3] = bf16_hi(w.y);
                 kf[4] = bf16_lo(w.z); kf[5] = bf16_hi(w.z);
@@ -165,13 +166,15 @@ __device__ __forceinline__ float lane_group_sum(float x) {
 template <bool BF16, int NC, int NJ>
 __global__ __launch_bounds__(kClsThreads) void cls_stream_kernel(
     Prob p, const void* __restrict__ qv, const void* __restrict__ kv,
-    float* __restrict__ logits, float2* __restrict__ stats, int kpw, int nchunks, int nc)
+    float* __restrict__ logits, float2* __restrict__ stats, int kpw, int nchunks, int nc,
+    Finish fin)
 {
     constexpr int CE = BF16 ? 8 : 4;                 // elements per 16-byte chunk
     constexpr int KB = 4;                            // key rows in flight per wave
     constexpr int NW = kClsThreads / kWave;
     __shared__ float red_m[NW][64], red_z[NW][64];
     const int c = blockIdx.x, b = blockIdx.y;
+    if (c == 0 && b == 0) clear_done(fin, p.B);      // counters of the cls_scores launch
     const int S = keys_of(p, b);
     const int s0 = c * kpw;
     if (s0 >= S) return;                             // uniform over the workgroup
@@ -227,7 +230,7 @@ __global__ __launch_bounds__(kClsThreads) void cls_stream_kernel(
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
                 float kf[CE];
-                if (BF16) {
+                if constexpr (BF16) {
                     kf[0] = bf16_lo(w[i][j].x); kf[1] = bf16_hi(w[i][j].x);
                     kf[2] = bf16_lo(w[i][j].y); kf[3] = bf16_hi(w[i][j].y);
                     kf[4] = bf16_lo(w[i][j].z); kf[5] = bf16_hi(w[i][j].z);
@@ -275,10 +278,13 @@ __global__ __launch_bounds__(kClsThreads) void cls_stream_kernel(
     }
 }
 
+// With fin.done (occam_prune) the last workgroup of each sample applies the threshold
+// and the compaction to the sample's scores (select_kernel's arithmetic).
 template <bool BF16>
 __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
     Prob p, const float* __restrict__ logits, const float2* __restrict__ stats,
-    const float* __restrict__ row_lse, float* __restrict__ scores, int kpw, int nchunks)
+    const float* __restrict__ row_lse, float* __restrict__ scores, int kpw, int nchunks,
+    Finish fin)
 {
     __shared__ float red_m[kClsThreads], red_z[kClsThreads];
     __shared__ float mh[64], izh[64];
@@ -333,8 +339,14 @@ __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
     for (int key = threadIdx.x; key < nk; key += blockDim.x) {
         float acc = 0.f;
         for (int h = 0; h < H; ++h) acc += cls_exp<BF16>(lrow[key * H + h] - mh[h]) * izh[h];
-        out[key] = acc * invH;
+        // Read by the sample's last workgroup in this launch: a device-coherent store.
+        if (fin.done) st_cc(out + key, acc * invH);
+        else out[key] = acc * invH;
     }
+    if (!fin.done) return;
+    char* lds = reinterpret_cast<char*>(red_m);
+    if (last_of_sample(fin.done, b, (unsigned)nch, reinterpret_cast<int*>(lds + 64)))
+        select_sample(p, scores, b, fin, lds + 128);
 }
 
 static size_t cls_logits_smem(const Prob& p, int bf16, int kpw) {
@@ -345,61 +357,64 @@ static size_t cls_logits_smem(const Prob& p, int bf16, int kpw) {
 
 template <bool BF16, int NC>
 static hipError_t cls_stream_launch(const Prob& p, const void* q, const void* k, float* logits,
-                                    float2* stats, int kpw, hipStream_t s) {
+                                    float2* stats, int kpw, const Finish& fin, hipStream_t s) {
     const int nc = p.d * (BF16 ? 2 : 4) / 16;
     const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
     dim3 grid(nchunks, p.B);
     const dim3 blk(kClsThreads);
     switch (NC * p.Hkv / 64) {
-    case 1: return launch(cls_stream_kernel<BF16, NC, 1>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc);
-    case 2: return launch(cls_stream_kernel<BF16, NC, 2>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc);
-    case 3: return launch(cls_stream_kernel<BF16, NC, 3>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc);
-    case 4: return launch(cls_stream_kernel<BF16, NC, 4>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc);
+    case 1: return launch(cls_stream_kernel<BF16, NC, 1>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc, fin);
+    case 2: return launch(cls_stream_kernel<BF16, NC, 2>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc, fin);
+    case 3: return launch(cls_stream_kernel<BF16, NC, 3>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc, fin);
+    case 4: return launch(cls_stream_kernel<BF16, NC, 4>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, nc, fin);
     default: return hipErrorInvalidValue;
     }
 }
 
 template <bool BF16>
 static hipError_t cls_stream_nc_launch(const Prob& p, int nc, const void* q, const void* k,
-                                       float* logits, float2* stats, int kpw, hipStream_t s) {
+                                       float* logits, float2* stats, int kpw, const Finish& fin,
+                                       hipStream_t s) {
     switch (nc) {
-    case 1: return cls_stream_launch<BF16, 1>(p, q, k, logits, stats, kpw, s);
-    case 2: return cls_stream_launch<BF16, 2>(p, q, k, logits, stats, kpw, s);
-    case 4: return cls_stream_launch<BF16, 4>(p, q, k, logits, stats, kpw, s);
-    case 8: return cls_stream_launch<BF16, 8>(p, q, k, logits, stats, kpw, s);
-    case 16: return cls_stream_launch<BF16, 16>(p, q, k, logits, stats, kpw, s);
+    case 1: return cls_stream_launch<BF16, 1>(p, q, k, logits, stats, kpw, fin, s);
+    case 2: return cls_stream_launch<BF16, 2>(p, q, k, logits, stats, kpw, fin, s);
+    case 4: return cls_stream_launch<BF16, 4>(p, q, k, logits, stats, kpw, fin, s);
+    case 8: return cls_stream_launch<BF16, 8>(p, q, k, logits, stats, kpw, fin, s);
+    case 16: return cls_stream_launch<BF16, 16>(p, q, k, logits, stats, kpw, fin, s);
     default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void* k,
-                             float* logits, float2* stats, int kpw, hipStream_t s)
+                             float* logits, float2* stats, int kpw, const Finish& fin,
+                             hipStream_t s)
 {
     const int nc = cls_stream_nc(p.H, p.Hkv, p.d, bf16 ? 2 : 4);
     if (nc) {
-        return bf16 ? cls_stream_nc_launch<true>(p, nc, q, k, logits, stats, kpw, s)
-                    : cls_stream_nc_launch<false>(p, nc, q, k, logits, stats, kpw, s);
+        return bf16 ? cls_stream_nc_launch<true>(p, nc, q, k, logits, stats, kpw, fin, s)
+                    : cls_stream_nc_launch<false>(p, nc, q, k, logits, stats, kpw, fin, s);
     }
     const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
     dim3 grid(nchunks, p.B);
     const size_t smem = cls_logits_smem(p, bf16, kpw);
     if (bf16)
         return launch(cls_logits_kernel<true>, grid, dim3(kClsThreads), smem, s, p, q, k, logits,
-                      stats, kpw, nchunks);
+                      stats, kpw, nchunks, fin);
     return launch(cls_logits_kernel<false>, grid, dim3(kClsThreads), smem, s, p, q, k, logits,
-                  stats, kpw, nchunks);
+                  stats, kpw, nchunks, fin);
 }
 
 hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const float2* stats,
-                             const float* row_lse, float* scores, int kpw, hipStream_t s)
+                             const float* row_lse, float* scores, int kpw, const Finish& fin,
+                             hipStream_t s)
 {
     const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
     dim3 grid(nchunks, p.B);
     if (bf16)
         return launch(cls_scores_kernel<true>, grid, dim3(kClsThreads), 0, s, p, logits, stats,
-                      row_lse, scores, kpw, nchunks);
+                      row_lse, scores, kpw, nchunks, fin);
     return launch(cls_scores_kernel<false>, grid, dim3(kClsThreads), 0, s, p, logits, stats,
-                  row_lse, scores, kpw, nchunks);
+                  row_lse, scores, kpw, nchunks, fin);
 }
 
 }  // namespace occam

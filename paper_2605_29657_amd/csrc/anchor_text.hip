@@ -117,17 +117,17 @@ __device__ __forceinline__ void wait_vmem_le() {
 // fixed-order sum over the partials (text_colsum_reduce).  Both modes stream the keys
 // the same way; the column sums use the MFMA the other way round (rows as the A
 // operand), so that a lane holds 16 rows of one key and sums them in registers.
-template <int DS, bool HALF, bool COLSUM, int RG>
-__global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
-    Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+template <int DS, bool HALF, bool COLSUM, int RG, int RING>
+__device__ __forceinline__ void stats_task(
+    const Prob& p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     float* __restrict__ lse2, const float* __restrict__ lse_in, int lse_natural,
-    float* __restrict__ part)
+    float* __restrict__ part, int b, int h, int tblk, char* smem_raw)
 {
     // kStatsThreads / 64 waves in kStreams key streams of RG waves each: wave w owns the
     // RPW = 128 / RG rows [rg*RPW, +RPW) of the row block (rg = w % RG) and the key
     // stream ks = w / RG (key blocks kbi = ks mod kStreams).  The RG waves of a stream
     // consume the same key blocks, so each block is copied once per stream, global ->
-    // LDS, into a ring of kStatsRing stages per stream: kStatsRing - 1 blocks are in
+    // LDS, into a ring of RING stages per stream: RING - 1 blocks are in
     // flight while one is used.  RG = 4 (32 rows per wave) needs half the registers of
     // RG = 2 and runs more waves per SIMD; the launcher uses it for every row count.
     // A block is 32 keys x NCH 16-byte chunks; chunk c of key j sits in LDS unit
@@ -144,16 +144,10 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     constexpr int MINE = (COPIES + RG - 1) / RG;     // most copies a stream member issues
     constexpr int MINE_MIN = COPIES / RG;            // fewest copies a stream member issues
     constexpr int SW = (NCH & (NCH - 1)) == 0 ? NCH - 1 : 0;
-    extern __shared__ __attribute__((aligned(16))) char smem_raw[];
     u32x4* ring = reinterpret_cast<u32x4*>(smem_raw);              // [stream][stage][UNITS]
-    float* red_m = reinterpret_cast<float*>(ring + kStreams * kStatsRing * UNITS);
+    float* red_m = reinterpret_cast<float*>(ring + kStreams * RING * UNITS);
     float* red_z = red_m + kStreams * kTxtRows;
-
-    // Task = (sample, head, row block), row blocks fastest, XCD-aware: the row blocks of
-    // one (sample, head) read the same keys and meet in one L2.
     const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
-    const int task = xcd_remap((int)blockIdx.x, nrb * p.H * p.B);
-    const int tblk = task % nrb, h = (task / nrb) % p.H, b = task / (nrb * p.H);
     const int T = rows_of(p, b);
     const int t0 = tblk * kTxtRows;
     if (t0 >= T) return;
@@ -203,7 +197,7 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
     const int nmine = (nkb - ks + kStreams - 1) / kStreams;     // blocks of this stream
     const char* kbase = reinterpret_cast<const char*>(k + ((size_t)kb0 * Hkv + g) * d);
     const int kstride = Hkv * d;                      // elements per key row
-    u32x4* sring = ring + ks * kStatsRing * UNITS;
+    u32x4* sring = ring + ks * RING * UNITS;
     const uint32_t sring_lds = lds_addr(sring);
 
     // Copy block j of this stream (clamped to the stream's last block) into its stage.
@@ -225,7 +219,7 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
         // every copy stays inside the sample's keys, and the stage is never read.
         const int kbi = min(ks + jj * kStreams, nkb - 1);
         const char* bbase = kbase + (size_t)kbi * 32 * kstride * 2;
-        const uint32_t dst = sring_lds + (uint32_t)((jj % kStatsRing) * UNITS * 16);
+        const uint32_t dst = sring_lds + (uint32_t)((jj % RING) * UNITS * 16);
         const bool full = kbi * 32 + 32 <= S;
 #pragma unroll
         for (int i = 0; i < MINE; ++i) {
@@ -359,17 +353,17 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
         }
     };
 #pragma unroll
-    for (int j = 0; j < kStatsRing - 1; ++j) issue(j);
+    for (int j = 0; j < RING - 1; ++j) issue(j);
     for (int i = 0; i < iters; ++i) {
-        // Own copies of block i have landed once at most kStatsRing-2 later blocks remain
+        // Own copies of block i have landed once at most RING-2 later blocks remain
         // (counted with the fewest copies a member issues: a stronger wait for the others).
-        wait_vmem_le<(kStatsRing - 2) * MINE_MIN>();
+        wait_vmem_le<(RING - 2) * MINE_MIN>();
         __syncthreads();                 // partner's copies landed; stage (i-1) is free
-        issue(i + kStatsRing - 1);
+        issue(i + RING - 1);
         if (COLSUM && rg == 0 && i >= 1 && i - 1 < nmine) store_sums(i - 1);
         if (i < nmine) {
             float cs = 0.f;
-            if (nsb > 0) cs = block(ks + i * kStreams, sring + (i % kStatsRing) * UNITS, i == 0);
+            if (nsb > 0) cs = block(ks + i * kStreams, sring + (i % RING) * UNITS, i == 0);
             if (COLSUM && hi == 0) sums[((i & 1) * kStreams + ks) * (RG * 32) + rg * 32 + lo] = cs;
         }
     }
@@ -399,6 +393,25 @@ __global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
         const int t = t0 + i;
         if (t < T) lse2[(size_t)(qb + t) * H + h] = mm + __builtin_amdgcn_logf(zz);
     }
+}
+
+// One statistics task per workgroup.  Task = (sample, head, row block), row blocks
+// fastest, XCD-aware: the row blocks of one (sample, head) read the same keys and meet in
+// one L2.
+// Workgroup 0 also clears the per-sample counters of the scoring kernel that follows.
+template <int DS, bool HALF, bool COLSUM, int RG>
+__global__ __launch_bounds__(kStatsThreads, 1) void text_stats_kernel(
+    Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    float* __restrict__ lse2, const float* __restrict__ lse_in, int lse_natural,
+    float* __restrict__ part, Finish fin)
+{
+    extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+    if (blockIdx.x == 0) clear_done(fin, p.B);
+    const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
+    const int task = xcd_remap((int)blockIdx.x, nrb * p.H * p.B);
+    const int tblk = task % nrb, h = (task / nrb) % p.H, b = task / (nrb * p.H);
+    stats_task<DS, HALF, COLSUM, RG, kStatsRing>(p, q, k, lse2, lse_in, lse_natural, part, b, h,
+                                                 tblk, smem_raw);
 }
 
 // Ragged launches: workgroup id -> the id-th non-empty (sample, key chunk, row block)
@@ -446,11 +459,16 @@ __device__ void ragged_score_task(const Prob& p, int id, int* sh) {
     }
 }
 
-template <int DS, bool HALF, bool FULL>
-__global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
-    Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+// One scoring task: keys [128 c, 128 c + 128) of sample b against its row block rb.
+// CC: the normalisers were written earlier in the same launch (by other workgroups), so
+// they are read with device-coherent loads.  cc_out: the scores / partials are read later
+// in the same launch by another workgroup, so they are written with device-coherent
+// stores.  rot_id spreads the starting heads.
+template <int DS, bool HALF, bool FULL, bool CC>
+__device__ __forceinline__ void score_task(
+    const Prob& p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     const float* __restrict__ lse, int lse_natural, float* __restrict__ scores,
-    float* __restrict__ part)
+    float* __restrict__ part, int b, int c, int rb, int rot_id, char* smem_raw, bool cc_out)
 {
     // 4 waves: wave w owns the 32 keys [s_lo + 32 w, +32) and the 128 rows of the
     // workgroup's row block (4 sub-blocks of 32 rows, one MFMA accumulator chain each).  Two workgroups share a CU, so one workgroup's MFMAs
@@ -468,36 +486,12 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     constexpr int QTILE = kTxtRows * NCH;                         // 16-byte units per tile
     constexpr int COPIES = QTILE / kWave / (kScoreThreads / kWave);  // per wave per tile
     constexpr int SW = (NCH & (NCH - 1)) == 0 ? NCH - 1 : 0;
-    extern __shared__ __attribute__((aligned(16))) char smem_raw[];
     u32x4* qt = reinterpret_cast<u32x4*>(smem_raw);                         // [2][QTILE]
     float* l2t = reinterpret_cast<float*>(smem_raw + 2 * QTILE * 16);       // [H][128]
-
-    // Task = (sample, key chunk, row block), row blocks fastest, XCD-aware: the chunks
-    // of one sample run on one XCD and share its L2 for the query tiles, and the row
-    // blocks of one chunk read the same keys there.  Samples in reverse order: the
-    // statistics pass streamed sample B-1 last, so its keys are the likeliest to still
-    // sit in the memory-side cache.  With several row blocks (part != null) each writes
-    // its row maximum (visual keys) or row sum (registers) to part[b][row block][key]
-    // and text_rows_combine forms the scores.
-    const int nchunk = (p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg;
+    // With several row blocks (part != null) each task writes its row maximum (visual
+    // keys) or row sum (registers) to part[b][row block][key]; the scores are formed from
+    // them afterwards (text_rows_combine, or the last task of the sample).
     const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
-    int b, c, rb;
-    if (p.k_off || p.q_off) {
-        // The decoded task passes through the start of query buffer 1, which is first
-        // written (head 1's copy) after the barrier that ends the prologue.
-        int* sh = reinterpret_cast<int*>(qt + QTILE);
-        if (threadIdx.x < kWave) ragged_score_task(p, (int)blockIdx.x, sh);
-        __syncthreads();
-        b = sh[0];
-        if (b < 0) return;
-        c = sh[1];
-        rb = sh[2];
-    } else {
-        const int task = xcd_remap((int)blockIdx.x, nchunk * nrb * p.B);
-        rb = task % nrb;
-        c = (task / nrb) % nchunk;
-        b = p.B - 1 - task / (nrb * nchunk);
-    }
     const int S = keys_of(p, b);
     const int s_lo = c * kTxtKeysPerWg;
     const int t0 = rb * kTxtRows;
@@ -519,7 +513,7 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     // serves the other workgroups' tile reads.  Steps past the last head repeat the
     // last one (clamped prefetches).
     const int nrot = H < 8 ? H : 8;
-    const int rot = (int)(blockIdx.x % (unsigned)nrot) * (H / nrot);
+    const int rot = (int)((unsigned)rot_id % (unsigned)nrot) * (H / nrot);
     auto head_of = [&](int hh) {
         const int hc = min(hh, H - 1) + rot;
         return hc >= H ? hc - H : hc;
@@ -577,7 +571,8 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
             const int hh = i / kTxtRows, t = t0 + (i % kTxtRows);
             float v = INFINITY;
             if (t < T) {
-                v = lse[(size_t)(qb + t) * H + hh];
+                const float* src = lse + (size_t)(qb + t) * H + hh;
+                v = CC ? __hip_atomic_load(src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : *src;
                 if (lse_natural) v *= kLog2e;
             }
             l2t[i] = v;
@@ -689,10 +684,77 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
         for (int r = 0; r < 16; ++r) {
             const int key = wkey0 + acc_key(r, hi);
             if (key >= S) continue;
-            if (prow) prow[key] = key < R ? sm[r] : mx[r];
-            else scores[kb0 + key] = key < R ? sm[r] * invHT : mx[r] * invH;
+            float* dst = prow ? prow + key : scores + kb0 + key;
+            const float v = prow ? (key < R ? sm[r] : mx[r]) : (key < R ? sm[r] * invHT : mx[r] * invH);
+            if (cc_out) st_cc(dst, v);
+            else *dst = v;
         }
     }
+}
+
+// One scoring task per workgroup.  Task = (sample, key chunk, row block), row blocks
+// fastest, XCD-aware: the chunks of one sample run on one XCD and share its L2 for the
+// query tiles, and the row blocks of one chunk read the same keys there.  Samples in
+// reverse order: the statistics pass streamed sample B-1 last, so its keys are the
+// likeliest to still sit in the memory-side cache.
+// With fin.done, the last workgroup of each sample forms its scores from the row blocks'
+// partials (text_rows_combine's arithmetic) and, with fin.select, applies the threshold
+// and the compaction (select_kernel's arithmetic).
+template <int DS, bool HALF, bool FULL>
+__global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
+    Prob p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
+    const float* __restrict__ lse, int lse_natural, float* __restrict__ scores,
+    float* __restrict__ part, Finish fin)
+{
+    extern __shared__ __attribute__((aligned(16))) char smem_raw[];
+    const int nchunk = (p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg;
+    const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
+    int b, c, rb;
+    if (p.k_off || p.q_off) {
+        // The decoded task passes through the start of query buffer 1 (after the first
+        // 128 x d tile), which is first written (head 1's copy) after the barrier that
+        // ends the task's prologue.
+        int* sh = reinterpret_cast<int*>(smem_raw + (size_t)kTxtRows * 2 * DS * 16);
+        if (threadIdx.x < kWave) ragged_score_task(p, (int)blockIdx.x, sh);
+        __syncthreads();
+        b = sh[0];
+        if (b < 0) return;
+        c = sh[1];
+        rb = sh[2];
+    } else {
+        const int task = xcd_remap((int)blockIdx.x, nchunk * nrb * p.B);
+        rb = task % nrb;
+        c = (task / nrb) % nchunk;
+        b = p.B - 1 - task / (nrb * nchunk);
+    }
+    score_task<DS, HALF, FULL, false>(p, q, k, lse, lse_natural, scores, part, b, c, rb,
+                                      (int)blockIdx.x, smem_raw, fin.done != nullptr);
+    if (!fin.done) return;
+    const int S = keys_of(p, b), T = rows_of(p, b);
+    const int nrb_b = (T + kTxtRows - 1) / kTxtRows;
+    const unsigned ntask = (unsigned)(((S + kTxtKeysPerWg - 1) / kTxtKeysPerWg) * nrb_b);
+    if (!last_of_sample(fin.done, b, ntask, reinterpret_cast<int*>(smem_raw + 64))) return;
+    if (part) {
+        // Row maxima (visual keys) / row sums (registers) over the row blocks in order,
+        // then the head (and row) mean.
+        const size_t smax = (size_t)(p.R + p.max_cands);
+        const float* pb = part + (size_t)b * nrb * smax;
+        float* out = scores + k_begin(p, b);
+        for (int s = threadIdx.x; s < S; s += kScoreThreads) {
+            float v = 0.f;
+            if (s < p.R) {
+                for (int r = 0; r < nrb_b; ++r) v += ld<true>(pb + (size_t)r * smax + s);
+                v *= 1.f / ((float)p.H * (float)T);
+            } else {
+                for (int r = 0; r < nrb_b; ++r) v = fmaxf(v, ld<true>(pb + (size_t)r * smax + s));
+                v *= 1.f / (float)p.H;
+            }
+            st_cc(out + s, v);          // read back below with coherent loads
+        }
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+        __syncthreads();
+    }
+    if (fin.select) select_sample(p, scores, b, fin, smem_raw + 128);
 }
 
 // Scores from the row blocks' partials: the maximum over row blocks (visual keys) or
@@ -719,7 +781,8 @@ __global__ __launch_bounds__(256) void text_rows_combine_kernel(Prob p, const fl
 
 template <int DS, bool HALF, bool COLSUM, int RG>
 static hipError_t stats_launch_rg(const Prob& p, const void* q, const void* k, float* lse2,
-                                  const float* lse_in, int lse_natural, float* part, hipStream_t s) {
+                                  const float* lse_in, int lse_natural, float* part,
+                                  const Finish& fin, hipStream_t s) {
     const size_t smem = text_stats_smem(DS * 16, RG);
     static std::atomic<uint64_t> lds_set{0};
     const hipError_t attr = allow_lds(
@@ -729,7 +792,7 @@ static hipError_t stats_launch_rg(const Prob& p, const void* q, const void* k, f
     dim3 grid((p.max_rows + kTxtRows - 1) / kTxtRows * p.H * p.B);
     return launch(text_stats_kernel<DS, HALF, COLSUM, RG>, grid, dim3(kStatsThreads), smem, s, p,
                   static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse2, lse_in,
-                  lse_natural, part);
+                  lse_natural, part, fin);
 }
 
 // Four waves of 32 rows on one key stream.  Two streams of two 64-row waves reuse each
@@ -737,19 +800,21 @@ static hipError_t stats_launch_rg(const Prob& p, const void* q, const void* k, f
 // 128, LLaVA-NeXT) the one-stream form measured 6 % faster (137-139 against 146-147 us).
 template <int DS, bool HALF, bool COLSUM>
 static hipError_t stats_launch(const Prob& p, const void* q, const void* k, float* lse2,
-                               const float* lse_in, int lse_natural, float* part, hipStream_t s) {
-    return stats_launch_rg<DS, HALF, COLSUM, 4>(p, q, k, lse2, lse_in, lse_natural, part, s);
+                               const float* lse_in, int lse_natural, float* part,
+                               const Finish& fin, hipStream_t s) {
+    return stats_launch_rg<DS, HALF, COLSUM, 4>(p, q, k, lse2, lse_in, lse_natural, part, fin, s);
 }
 
 template <int DS, bool HALF>
-static hipError_t stats_ds(const Prob& p, const void* q, const void* k, float* lse2, hipStream_t s) {
-    return stats_launch<DS, HALF, false>(p, q, k, lse2, nullptr, 0, nullptr, s);
+static hipError_t stats_ds(const Prob& p, const void* q, const void* k, float* lse2,
+                           const Finish& fin, hipStream_t s) {
+    return stats_launch<DS, HALF, false>(p, q, k, lse2, nullptr, 0, nullptr, fin, s);
 }
 
 template <int DS, bool HALF>
 static hipError_t colsum_ds(const Prob& p, const void* q, const void* k, const float* lse,
                             int lse_natural, float* part, hipStream_t s) {
-    return stats_launch<DS, HALF, true>(p, q, k, nullptr, lse, lse_natural, part, s);
+    return stats_launch<DS, HALF, true>(p, q, k, nullptr, lse, lse_natural, part, Finish{}, s);
 }
 
 // Mutual scores: the mean over rows and heads of p, from the per-(row block, head)
@@ -781,7 +846,8 @@ __global__ __launch_bounds__(256) void text_colsum_reduce_kernel(Prob p, const f
 
 template <int DS, bool HALF, bool FULL>
 static hipError_t score_launch(const Prob& p, const void* q, const void* k, const float* lse,
-                               int lse_natural, float* scores, float* part, hipStream_t s) {
+                               int lse_natural, float* scores, float* part, const Finish& fin,
+                               hipStream_t s) {
     const size_t smem = text_score_smem(p.H, DS * 16);
     // The tile needs more than the default 64 KB of dynamic LDS: raise the limit (once per
     // device).
@@ -794,19 +860,21 @@ static hipError_t score_launch(const Prob& p, const void* q, const void* k, cons
     dim3 grid((p.R + p.max_cands + kTxtKeysPerWg - 1) / kTxtKeysPerWg * nrb * p.B);
     return launch(text_score_kernel<DS, HALF, FULL>, grid, dim3(kScoreThreads), smem, s, p,
                   static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k), lse,
-                  lse_natural, scores, nrb > 1 ? part : nullptr);
+                  lse_natural, scores, nrb > 1 ? part : nullptr, fin);
 }
 
 template <int DS, bool HALF>
 static hipError_t score_ds(const Prob& p, const void* q, const void* k, const float* lse,
-                           int lse_natural, float* scores, float* part, hipStream_t s) {
+                           int lse_natural, float* scores, float* part, const Finish& fin,
+                           hipStream_t s) {
     // Uniform rows that fill whole 128-row blocks take the pipelined form.
     const bool full = !p.q_off && p.rows == p.max_rows && p.rows % kTxtRows == 0;
-    const hipError_t e = full ? score_launch<DS, HALF, true>(p, q, k, lse, lse_natural, scores, part, s)
-                              : score_launch<DS, HALF, false>(p, q, k, lse, lse_natural, scores, part, s);
+    const hipError_t e =
+        full ? score_launch<DS, HALF, true>(p, q, k, lse, lse_natural, scores, part, fin, s)
+             : score_launch<DS, HALF, false>(p, q, k, lse, lse_natural, scores, part, fin, s);
     if (e != hipSuccess) return e;
     const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
-    if (nrb == 1) return hipSuccess;
+    if (nrb == 1 || fin.done) return hipSuccess;
     dim3 cgrid((p.R + p.max_cands + 255) / 256, p.B);
     return launch(text_rows_combine_kernel, cgrid, dim3(256), 0, s, p, part, scores);
 }
@@ -826,13 +894,14 @@ static hipError_t score_ds(const Prob& p, const void* q, const void* k, const fl
     }
 
 hipError_t launch_text_stats(const Prob& p, const void* q, const void* k, float* lse2,
-                             hipStream_t s) {
-    OCCAM_D_SWITCH(stats_ds, p, q, k, lse2, s)
+                             const Finish& fin, hipStream_t s) {
+    OCCAM_D_SWITCH(stats_ds, p, q, k, lse2, fin, s)
 }
 
 hipError_t launch_text_score(const Prob& p, const void* q, const void* k, const float* lse,
-                             int lse_natural, float* scores, float* part, hipStream_t s) {
-    OCCAM_D_SWITCH(score_ds, p, q, k, lse, lse_natural, scores, part, s)
+                             int lse_natural, float* scores, float* part, const Finish& fin,
+                             hipStream_t s) {
+    OCCAM_D_SWITCH(score_ds, p, q, k, lse, lse_natural, scores, part, fin, s)
 }
 
 static hipError_t colsum_any(const Prob& p, const void* q, const void* k, const float* lse,

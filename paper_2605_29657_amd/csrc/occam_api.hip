@@ -23,7 +23,8 @@ struct Plan {
     int bf16;
     int text;          // 1: several anchor rows (MFMA path); 0: one anchor row (VALU path)
     int kpw;           // keys per workgroup of the one-row path
-    size_t off_logits, off_stats, off_lse2, off_part, off_scores, off_tau, off_slot, off_match, total;
+    size_t off_logits, off_stats, off_lse2, off_part, off_done, off_scores, off_tau, off_slot,
+        off_match, total;
 };
 
 bool aligned(const void* ptr, size_t a) { return (reinterpret_cast<uintptr_t>(ptr) % a) == 0; }
@@ -95,6 +96,8 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
         P.off_logits = off; off = align_up(off + (size_t)keys_cap * H * sizeof(float));
         P.off_stats = off; off = align_up(off + (size_t)B * nchunks * H * sizeof(float2));
     }
+    // Finished workgroups per sample (the in-kernel threshold / compaction epilogue).
+    P.off_done = off; off = align_up(off + (size_t)B * sizeof(unsigned));
     P.off_scores = off; off = align_up(off + (size_t)keys_cap * sizeof(float));
     P.off_tau = off; off = align_up(off + (size_t)B * sizeof(float));
     P.off_slot = off; off = align_up(off + (size_t)B * max_cands * sizeof(int));
@@ -151,27 +154,42 @@ occam_status rows_from(int32_t n, const occam_rows* t, RowTensors* out) {
 
 inline occam_status hip_ok(hipError_t e) { return e == hipSuccess ? OCCAM_OK : OCCAM_ERR_HIP; }
 
-// Steps 1-2 into `scores` (device), both paths.
+// Steps 1-2 into `scores` (device), both paths.  With `sel` (occam_prune) the threshold and
+// the compaction are applied as well, inside the scoring kernel, wherever the call has a
+// kernel before it that clears the per-sample counters (the one-row logits; the text-row
+// statistics, i.e. no caller normaliser): then *selected is set.  The multi-row max form
+// then also combines its row blocks in the scoring kernel.
 occam_status run_score(const Plan& P, const void* q, const void* k, const float* row_lse,
-                       float* scores, void* ws, hipStream_t s) {
+                       float* scores, void* ws, hipStream_t s, const Finish* sel = nullptr,
+                       int* selected = nullptr) {
+    Finish fin{};
+    if (selected) *selected = 0;
+    const bool counters = !P.text || (!row_lse && !P.p.mean_rows);
+    const bool combine = P.text && P.p.max_rows > kTxtRows;     // several row blocks
+    if (counters && (sel || combine)) {
+        if (sel) fin = *sel;
+        fin.done = ws_at<unsigned>(ws, P.off_done);
+        fin.select = sel ? 1 : 0;
+        if (selected) *selected = fin.select;
+    }
     if (P.text) {
         const float* lse = row_lse;
         if (!row_lse) {
             float* lse2 = ws_at<float>(ws, P.off_lse2);
-            occam_status st = hip_ok(launch_text_stats(P.p, q, k, lse2, s));
+            occam_status st = hip_ok(launch_text_stats(P.p, q, k, lse2, fin, s));
             if (st != OCCAM_OK) return st;
             lse = lse2;
         }
         const int natural = row_lse ? 1 : 0;
         float* part = ws_at<float>(ws, P.off_part);
         if (P.p.mean_rows) return hip_ok(launch_text_colsum(P.p, q, k, lse, natural, part, scores, s));
-        return hip_ok(launch_text_score(P.p, q, k, lse, natural, scores, part, s));
+        return hip_ok(launch_text_score(P.p, q, k, lse, natural, scores, part, fin, s));
     }
     float* logits = ws_at<float>(ws, P.off_logits);
     float2* stats = ws_at<float2>(ws, P.off_stats);
-    occam_status st = hip_ok(launch_cls_logits(P.p, P.bf16, q, k, logits, stats, P.kpw, s));
+    occam_status st = hip_ok(launch_cls_logits(P.p, P.bf16, q, k, logits, stats, P.kpw, fin, s));
     if (st != OCCAM_OK) return st;
-    return hip_ok(launch_cls_scores(P.p, P.bf16, logits, stats, row_lse, scores, P.kpw, s));
+    return hip_ok(launch_cls_scores(P.p, P.bf16, logits, stats, row_lse, scores, P.kpw, fin, s));
 }
 
 // The key layout of a problem alone (register construction reads no anchor rows).
@@ -223,9 +241,19 @@ occam_status run_prune(const Plan& P, const void* q, const void* k, const float*
     float* sc = scores ? scores : ws_at<float>(workspace, P.off_scores);
     float* tu = tau ? tau : ws_at<float>(workspace, P.off_tau);
     int* slot = ws_at<int>(workspace, P.off_slot);
-    if ((st = run_score(P, q, k, row_lse, sc, workspace, stream)) != OCCAM_OK) return st;
-    st = hip_ok(launch_select(P.p, sc, nullptr, 1, lambda, reduce, tu, slot, kept_count, stream));
-    if (st != OCCAM_OK) return st;
+    Finish sel{};
+    sel.lambda = lambda;
+    sel.reduce = reduce;
+    sel.tau = tu;
+    sel.slot = slot;
+    sel.count = kept_count;
+    int selected = 0;
+    if ((st = run_score(P, q, k, row_lse, sc, workspace, stream, &sel, &selected)) != OCCAM_OK)
+        return st;
+    if (!selected) {
+        st = hip_ok(launch_select(P.p, sc, nullptr, 1, lambda, reduce, tu, slot, kept_count, stream));
+        if (st != OCCAM_OK) return st;
+    }
     return hip_ok(launch_pack_gather(P.p, slot, kept_count, index_map, kept_idx, kept_offsets,
                                      nullptr, nullptr, rows, stream));
 }

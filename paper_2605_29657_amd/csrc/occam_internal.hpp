@@ -49,6 +49,20 @@ constexpr int kMaxGridY = 65535;   // launch limit of grid.y (the sample index o
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 constexpr float kLog2e = 1.4426950408889634f;
 
+// Loads and stores of values that other workgroups of the same launch write or read
+// (possibly on other XCDs, each with its own L2): device-coherent when CC, i.e. they
+// bypass the non-coherent caches instead of needing a cache-wide write-back or
+// invalidation.
+template <bool CC, typename T>
+__device__ __forceinline__ T ld(const T* p) {
+    if constexpr (CC) return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else return *p;
+}
+template <typename T>
+__device__ __forceinline__ void st_cc(T* p, T v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
 // Problem view passed by value to every kernel.  Offsets are device pointers
 // or null (uniform batch).
 struct Prob {
@@ -86,14 +100,15 @@ __device__ __forceinline__ int cand_begin(const Prob& p, int b) {
 }
 
 // s_b(r): the register scores of one sample reduced by mean, max or sum.
+template <bool CC = false>
 __device__ __forceinline__ float reg_reduce(const float* s, int R, int reduce) {
     if (reduce == 1) {                     // OCCAM_REG_MAX
-        float m = s[0];
-        for (int r = 1; r < R; ++r) m = fmaxf(m, s[r]);
+        float m = ld<CC>(s);
+        for (int r = 1; r < R; ++r) m = fmaxf(m, ld<CC>(s + r));
         return m;
     }
     float acc = 0.f;
-    for (int r = 0; r < R; ++r) acc += s[r];
+    for (int r = 0; r < R; ++r) acc += ld<CC>(s + r);
     return reduce == 0 ? acc / (float)R : acc;   // MEAN : SUM
 }
 
@@ -105,17 +120,17 @@ constexpr int kRefCandMean = 3;            // OCCAM_REF_CAND_MEAN
 // threads, a fixed shuffle tree per wave, the waves in order; threads past NT take no
 // part), so every kernel that calls it with the same NT gets the same bits, whatever
 // its workgroup size.  `red` is NT / 64 floats of LDS.
-template <int NT>
+template <int NT, bool CC = false>
 __device__ __forceinline__ float sample_reference(const Prob& p, const float* scores, int b,
                                                   int reduce, float* red) {
     const int kb = k_begin(p, b);
-    if (reduce != kRefCandMean) return reg_reduce(scores + kb, p.R, reduce);
+    if (reduce != kRefCandMean) return reg_reduce<CC>(scores + kb, p.R, reduce);
     const int N = keys_of(p, b) - p.R;
     const float* sv = scores + kb + p.R;
     const bool part = threadIdx.x < NT;
     float acc = 0.f;
     if (part)
-        for (int v = threadIdx.x; v < N; v += NT) acc += sv[v];
+        for (int v = threadIdx.x; v < N; v += NT) acc += ld<CC>(sv + v);
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
     __syncthreads();                          // `red` may still be read by a previous call
@@ -125,6 +140,44 @@ __device__ __forceinline__ float sample_reference(const Prob& p, const float* sc
 #pragma unroll
     for (int w = 0; w < NT / 64; ++w) sum += red[w];
     return N > 0 ? sum / (float)N : 0.f;
+}
+
+// Ascending compaction of sample b's survivors (scores[kb + R + v] >= tau) into
+// slot[co_b + i] and count[b], by a workgroup of NT threads (all must call it): thread t
+// owns the contiguous strip [t*P, t*P + P) of the candidates, counts its survivors, one
+// block-wide exclusive scan (a shuffle scan per wave, then the NT/64 wave totals in
+// order) gives every strip its output position, and the strip writes its survivors in
+// ascending order.  The result does not depend on NT.  `wsum` is NT / 64 ints of LDS.
+template <int NT, bool CC = false>
+__device__ __forceinline__ void compact_sample(const Prob& p, const float* scores, int b,
+                                               float tau, int* slot, int* count, int* wsum) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int N = keys_of(p, b) - p.R;
+    const float* sv = scores + k_begin(p, b) + p.R;
+    const int P = (N + NT - 1) / NT;
+    const int v0 = min(N, tid * P), v1 = min(N, v0 + P);
+    int cnt = 0;
+    for (int v = v0; v < v1; ++v) cnt += ld<CC>(sv + v) >= tau ? 1 : 0;
+    int inc = cnt;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int o = __shfl_up(inc, off);
+        if (lane >= off) inc += o;
+    }
+    __syncthreads();                          // `wsum` may still be read by a previous call
+    if (lane == kWave - 1) wsum[wave] = inc;
+    __syncthreads();
+    int base = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < NT / kWave; ++w) {
+        base += w < wave ? wsum[w] : 0;
+        total += wsum[w];
+    }
+    int pos = base + inc - cnt;
+    int* out = slot + cand_begin(p, b);
+    for (int v = v0; v < v1; ++v)
+        if (ld<CC>(sv + v) >= tau) out[pos++] = v;
+    if (tid == 0) count[b] = total;
 }
 
 // Floats as unsigned keys with the same order: -0 folds into +0, non-negative values
@@ -230,6 +283,61 @@ inline int cls_keys_per_wg(int H, int Hkv, int d, int elem_bytes) {
     return kpw;
 }
 
+// Per-sample epilogue of occam_prune, run inside the scoring kernels by the last
+// workgroup to finish each sample (so that no separate threshold / select or row-block
+// combine launch is needed).  done[B] counts the finished workgroups of every sample; the
+// kernel that runs just before the scoring kernel in the same call clears it.  done ==
+// null: no epilogue.
+struct Finish {
+    unsigned* done;
+    int select;            // threshold + compaction (else only the row-block combine)
+    float lambda;
+    int reduce;
+    float* tau;            // [B], tau_b
+    int* slot;             // survivors, slot[co_b + i]
+    int* count;            // [B]
+};
+
+// Zero done[0 .. B) (one workgroup of the kernel that precedes the scoring kernel).
+__device__ __forceinline__ void clear_done(const Finish& f, int B) {
+    if (!f.done) return;
+    for (int i = threadIdx.x; i < B; i += blockDim.x) f.done[i] = 0u;
+}
+
+// Every thread of the workgroup calls this after writing its share of sample b's scores
+// (or row-block partials) with device-coherent stores (st_cc).  Each wave waits until its
+// stores have completed, the workgroup counts itself, and the one that completes the
+// sample's ntask workgroups gets true; it then reads the other workgroups' values with
+// device-coherent loads (ld<true>).  No cache-wide write-back or invalidation is needed
+// (measured: an agent-scope release/acquire fence pair in every workgroup of the Stage II
+// scoring kernel cost ~90 us per launch).  flag: one int of LDS.
+__device__ __forceinline__ bool last_of_sample(unsigned* done, int b, unsigned ntask, int* flag) {
+    __builtin_amdgcn_s_waitcnt(0x0F70);          // vmcnt(0): this wave's stores are done
+    __syncthreads();
+    if (threadIdx.x == 0)
+        *flag = __hip_atomic_fetch_add(done + b, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u ==
+                ntask;
+    __syncthreads();
+    return *flag != 0;
+}
+
+// Threshold (tau_b = lambda * reference, the fused threshold of select_kernel) and
+// compaction of sample b by one workgroup of kSelThreads threads, reading the scores with
+// device-coherent loads.  lds: 48 bytes.
+__device__ __forceinline__ void select_sample(const Prob& p, const float* scores, int b,
+                                              const Finish& f, char* lds) {
+    float* red = reinterpret_cast<float*>(lds);              // kSelThreads / 64 floats
+    int* wsum = reinterpret_cast<int*>(lds + 16);            // kSelThreads / 64 ints
+    float* tau_s = reinterpret_cast<float*>(lds + 32);
+    const float t = f.lambda * sample_reference<kSelThreads, true>(p, scores, b, f.reduce, red);
+    if (threadIdx.x == 0) {
+        if (f.tau) f.tau[b] = t;
+        *tau_s = t;
+    }
+    __syncthreads();
+    compact_sample<kSelThreads, true>(p, scores, b, *tau_s, f.slot, f.count, wsum);
+}
+
 // ---------------------------------------------------------------------------
 // Launchers (defined in the .hip files).  Each returns the status of its own launches.
 hipError_t launch_select_topk(const Prob& p, const float* scores, int k_keep, int* slot,
@@ -241,20 +349,27 @@ hipError_t launch_match_lambda(const Prob& p, const float* scores, int reduce, f
 hipError_t launch_register_redirect(const Prob& p, int bf16, void* h, int width, long long stride,
                                     const int* channels, int n_channels, int reg_slot,
                                     hipStream_t s);
+// fin.done (nullable) is cleared by launch_cls_logits / launch_text_stats and used by the
+// scoring launch that follows them in the same call.
 hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void* k,
-                             float* logits, float2* stats, int kpw, hipStream_t s);
-hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const float2* stats,
-                             const float* row_lse, float* scores, int kpw, hipStream_t s);
-hipError_t launch_text_stats(const Prob& p, const void* q, const void* k, float* lse2,
+                             float* logits, float2* stats, int kpw, const Finish& fin,
                              hipStream_t s);
+hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const float2* stats,
+                             const float* row_lse, float* scores, int kpw, const Finish& fin,
+                             hipStream_t s);
+hipError_t launch_text_stats(const Prob& p, const void* q, const void* k, float* lse2,
+                             const Finish& fin, hipStream_t s);
 // Mutual scoring (every key: mean over rows): column sums per (row block, head) into
 // part [B][ceil(max_rows/128)][H][R + max_cands], then their fixed-order mean.
 hipError_t launch_text_colsum(const Prob& p, const void* q, const void* k, const float* lse,
                               int lse_natural, float* part, float* scores, hipStream_t s);
 // Max-over-rows scoring; with several 128-row blocks, per-block partials go to part
 // [B][ceil(max_rows/128)][R + max_cands] and a combine kernel forms the scores.
+// With fin.done the row-block combine (and with fin.select the threshold and the
+// compaction) run in each sample's last workgroup; without it text_rows_combine follows.
 hipError_t launch_text_score(const Prob& p, const void* q, const void* k, const float* lse,
-                             int lse_natural, float* scores, float* part, hipStream_t s);
+                             int lse_natural, float* scores, float* part, const Finish& fin,
+                             hipStream_t s);
 hipError_t launch_threshold(const Prob& p, const float* scores, float lambda, int reduce,
                             float* tau, hipStream_t s);
 hipError_t launch_select(const Prob& p, const float* scores, const float* tau, int fuse_tau,

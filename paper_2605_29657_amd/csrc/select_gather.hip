@@ -43,54 +43,23 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(
     float lambda, int reduce, float* __restrict__ tau_out, int* __restrict__ slot,
     int* __restrict__ count)
 {
-    // Thread t owns the contiguous strip [t*P, t*P + P) of the sample's candidates:
-    // it counts its survivors, one block-wide exclusive scan gives every strip its
-    // output position, and the strip writes its survivors in ascending order.  The fused
-    // threshold's reference sum runs in the order of kSelThreads threads, the same bits
-    // as occam_threshold and budget matching.
+    // The fused threshold's reference sum runs in the order of kSelThreads threads, the
+    // same bits as occam_threshold and budget matching.
     __shared__ int wsum[kSelectThreads / kWave];
     __shared__ float red[kSelThreads / kWave];
     __shared__ float tau_s;
     const int b = blockIdx.x;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int kb = k_begin(p, b);
-    const int N = keys_of(p, b) - p.R;
-    const int co = cand_begin(p, b);
     if (fuse_tau) {
         const float t = lambda * sample_reference<kSelThreads>(p, scores, b, reduce, red);
-        if (tid == 0) {
+        if (threadIdx.x == 0) {
             if (tau_out) tau_out[b] = t;
             tau_s = t;
         }
-    } else if (tid == 0) {
+    } else if (threadIdx.x == 0) {
         tau_s = tau_in[b];
     }
     __syncthreads();
-    const float tau = tau_s;
-    const float* sv = scores + kb + p.R;
-    const int P = (N + kSelectThreads - 1) / kSelectThreads;
-    const int v0 = min(N, tid * P), v1 = min(N, v0 + P);
-    int cnt = 0;
-    for (int v = v0; v < v1; ++v) cnt += sv[v] >= tau ? 1 : 0;
-    // Inclusive scan inside the wave, then across the waves.
-    int inc = cnt;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const int o = __shfl_up(inc, off);
-        if (lane >= off) inc += o;
-    }
-    if (lane == kWave - 1) wsum[wave] = inc;
-    __syncthreads();
-    int base = 0, total = 0;
-#pragma unroll
-    for (int w = 0; w < kSelectThreads / kWave; ++w) {
-        base += w < wave ? wsum[w] : 0;
-        total += wsum[w];
-    }
-    int pos = base + inc - cnt;
-    for (int v = v0; v < v1; ++v)
-        if (sv[v] >= tau) slot[co + pos++] = v;
-    if (tid == 0) count[b] = total;
+    compact_sample<kSelectThreads>(p, scores, b, tau_s, slot, count, wsum);
 }
 
 __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
