@@ -344,9 +344,11 @@ __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
         else out[key] = acc * invH;
     }
     if (!fin.done) return;
-    char* lds = reinterpret_cast<char*>(red_m);
-    if (last_of_sample(fin.done, b, (unsigned)nch, reinterpret_cast<int*>(lds + 64)))
-        select_sample(p, scores, b, fin, lds + 128);
+    // Dynamic LDS (launched only with the epilogue): the counter flag, then the select
+    // scratch and the copy of the sample's scores.
+    extern __shared__ __attribute__((aligned(16))) char cls_dyn[];
+    if (last_of_sample(fin.done, b, (unsigned)nch, reinterpret_cast<int*>(cls_dyn)))
+        select_sample(p, scores, b, fin, cls_dyn + 64);
 }
 
 static size_t cls_logits_smem(const Prob& p, int bf16, int kpw) {
@@ -410,10 +412,11 @@ hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const
 {
     const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
     dim3 grid(nchunks, p.B);
+    const size_t smem = fin.done ? 64 + select_lds_bytes(p.R, p.max_cands) : 0;
     if (bf16)
-        return launch(cls_scores_kernel<true>, grid, dim3(kClsThreads), 0, s, p, logits, stats,
+        return launch(cls_scores_kernel<true>, grid, dim3(kClsThreads), smem, s, p, logits, stats,
                       row_lse, scores, kpw, nchunks, fin);
-    return launch(cls_scores_kernel<false>, grid, dim3(kClsThreads), 0, s, p, logits, stats,
+    return launch(cls_scores_kernel<false>, grid, dim3(kClsThreads), smem, s, p, logits, stats,
                   row_lse, scores, kpw, nchunks, fin);
 }
 

@@ -727,8 +727,11 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
         c = (task / nrb) % nchunk;
         b = p.B - 1 - task / (nrb * nchunk);
     }
+    // The starting head follows the key chunk, not the workgroup: the row blocks of one
+    // chunk (adjacent tasks, one XCD) then read the same key slices at about the same time
+    // and share them in L2 instead of each fetching the chunk's keys from memory.
     score_task<DS, HALF, FULL, false>(p, q, k, lse, lse_natural, scores, part, b, c, rb,
-                                      (int)blockIdx.x, smem_raw, fin.done != nullptr);
+                                      b * nchunk + c, smem_raw, fin.done != nullptr);
     if (!fin.done) return;
     const int S = keys_of(p, b), T = rows_of(p, b);
     const int nrb_b = (T + kTxtRows - 1) / kTxtRows;

@@ -166,10 +166,16 @@ occam_status run_score(const Plan& P, const void* q, const void* k, const float*
     if (selected) *selected = 0;
     const bool counters = !P.text || (!row_lse && !P.p.mean_rows);
     const bool combine = P.text && P.p.max_rows > kTxtRows;     // several row blocks
-    if (counters && (sel || combine)) {
+    // The epilogue copies a sample's scores into LDS: the scoring kernel's tiles hold it
+    // (text rows), or up to 48 KB of dynamic LDS (one row).
+    const size_t need = 128 + select_lds_bytes(P.p.R, P.p.max_cands);
+    const bool fits = P.text ? need <= text_score_smem(P.p.H, ((P.p.d + 15) / 16) * 16)
+                             : need <= 48 * 1024;
+    const bool do_select = sel && fits;
+    if (counters && (do_select || combine)) {
         if (sel) fin = *sel;
         fin.done = ws_at<unsigned>(ws, P.off_done);
-        fin.select = sel ? 1 : 0;
+        fin.select = do_select ? 1 : 0;
         if (selected) *selected = fin.select;
     }
     if (P.text) {

@@ -114,19 +114,18 @@ __device__ __forceinline__ float reg_reduce(const float* s, int R, int reduce) {
 
 constexpr int kRefCandMean = 3;            // OCCAM_REF_CAND_MEAN
 
-// Reference score of sample b, returned to every thread of a workgroup of at least NT
-// threads (all of them must call it).  Register reductions read the R register scores;
-// the candidate mean sums the visual scores in a fixed order (strided over the first NT
-// threads, a fixed shuffle tree per wave, the waves in order; threads past NT take no
-// part), so every kernel that calls it with the same NT gets the same bits, whatever
-// its workgroup size.  `red` is NT / 64 floats of LDS.
+// Reference score of one sample from its R + N scores s[0 .. R + N) (registers first),
+// returned to every thread of a workgroup of at least NT threads (all of them must call
+// it).  Register reductions read the R register scores; the candidate mean sums the visual
+// scores in a fixed order (strided over the first NT threads, a fixed shuffle tree per
+// wave, the waves in order; threads past NT take no part), so every kernel that calls it
+// with the same NT gets the same bits, whatever its workgroup size and wherever the scores
+// are held.  `red` is NT / 64 floats of LDS.
 template <int NT, bool CC = false>
-__device__ __forceinline__ float sample_reference(const Prob& p, const float* scores, int b,
-                                                  int reduce, float* red) {
-    const int kb = k_begin(p, b);
-    if (reduce != kRefCandMean) return reg_reduce<CC>(scores + kb, p.R, reduce);
-    const int N = keys_of(p, b) - p.R;
-    const float* sv = scores + kb + p.R;
+__device__ __forceinline__ float reference_of(const float* s, int R, int N, int reduce,
+                                              float* red) {
+    if (reduce != kRefCandMean) return reg_reduce<CC>(s, R, reduce);
+    const float* sv = s + R;
     const bool part = threadIdx.x < NT;
     float acc = 0.f;
     if (part)
@@ -142,22 +141,27 @@ __device__ __forceinline__ float sample_reference(const Prob& p, const float* sc
     return N > 0 ? sum / (float)N : 0.f;
 }
 
-// Ascending compaction of sample b's survivors (scores[kb + R + v] >= tau) into
-// slot[co_b + i] and count[b], by a workgroup of NT threads (all must call it): thread t
-// owns the contiguous strip [t*P, t*P + P) of the candidates, counts its survivors, one
-// block-wide exclusive scan (a shuffle scan per wave, then the NT/64 wave totals in
-// order) gives every strip its output position, and the strip writes its survivors in
-// ascending order.  The result does not depend on NT.  `wsum` is NT / 64 ints of LDS.
+// The reference of sample b read from the packed score array.
 template <int NT, bool CC = false>
-__device__ __forceinline__ void compact_sample(const Prob& p, const float* scores, int b,
-                                               float tau, int* slot, int* count, int* wsum) {
+__device__ __forceinline__ float sample_reference(const Prob& p, const float* scores, int b,
+                                                  int reduce, float* red) {
+    return reference_of<NT, CC>(scores + k_begin(p, b), p.R, keys_of(p, b) - p.R, reduce, red);
+}
+
+// Ascending compaction of a sample's survivors (sv[v] >= tau over its N visual scores)
+// into out[i] and *count, by a workgroup of NT threads (all must call it): thread t owns
+// the contiguous strip [t*P, t*P + P) of the candidates, counts its survivors, one
+// block-wide exclusive scan (a shuffle scan per wave, then the NT/64 wave totals in order)
+// gives every strip its output position, and the strip writes its survivors in ascending
+// order.  The result does not depend on NT.  `wsum` is NT / 64 ints of LDS.
+template <int NT>
+__device__ __forceinline__ void compact_of(const float* sv, int N, float tau, int* out,
+                                           int* count, int* wsum) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int N = keys_of(p, b) - p.R;
-    const float* sv = scores + k_begin(p, b) + p.R;
     const int P = (N + NT - 1) / NT;
     const int v0 = min(N, tid * P), v1 = min(N, v0 + P);
     int cnt = 0;
-    for (int v = v0; v < v1; ++v) cnt += ld<CC>(sv + v) >= tau ? 1 : 0;
+    for (int v = v0; v < v1; ++v) cnt += sv[v] >= tau ? 1 : 0;
     int inc = cnt;
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) {
@@ -174,10 +178,17 @@ __device__ __forceinline__ void compact_sample(const Prob& p, const float* score
         total += wsum[w];
     }
     int pos = base + inc - cnt;
-    int* out = slot + cand_begin(p, b);
     for (int v = v0; v < v1; ++v)
-        if (ld<CC>(sv + v) >= tau) out[pos++] = v;
-    if (tid == 0) count[b] = total;
+        if (sv[v] >= tau) out[pos++] = v;
+    if (tid == 0) *count = total;
+}
+
+// The compaction of sample b from the packed score array into slot[co_b + i], count[b].
+template <int NT>
+__device__ __forceinline__ void compact_sample(const Prob& p, const float* scores, int b,
+                                               float tau, int* slot, int* count, int* wsum) {
+    compact_of<NT>(scores + k_begin(p, b) + p.R, keys_of(p, b) - p.R, tau,
+                   slot + cand_begin(p, b), count + b, wsum);
 }
 
 // Floats as unsigned keys with the same order: -0 folds into +0, non-negative values
@@ -321,21 +332,48 @@ __device__ __forceinline__ bool last_of_sample(unsigned* done, int b, unsigned n
     return *flag != 0;
 }
 
+// LDS the per-sample epilogue needs: its scratch words and a copy of the sample's scores.
+constexpr size_t kSelectScratch = 64;
+inline size_t select_lds_bytes(int R, int max_cands) {
+    return kSelectScratch + 4 * ((size_t)R + (size_t)max_cands);
+}
+
 // Threshold (tau_b = lambda * reference, the fused threshold of select_kernel) and
-// compaction of sample b by one workgroup of kSelThreads threads, reading the scores with
-// device-coherent loads.  lds: 48 bytes.
+// compaction of sample b by one workgroup of kSelThreads threads.  The sample's scores,
+// written by other workgroups of the launch, are first copied into LDS with
+// device-coherent loads (eight in flight per thread); the reference and the compaction
+// then read the copy, with select_kernel's arithmetic.  lds: select_lds_bytes(R, N_b).
 __device__ __forceinline__ void select_sample(const Prob& p, const float* scores, int b,
                                               const Finish& f, char* lds) {
     float* red = reinterpret_cast<float*>(lds);              // kSelThreads / 64 floats
     int* wsum = reinterpret_cast<int*>(lds + 16);            // kSelThreads / 64 ints
     float* tau_s = reinterpret_cast<float*>(lds + 32);
-    const float t = f.lambda * sample_reference<kSelThreads, true>(p, scores, b, f.reduce, red);
+    float* sl = reinterpret_cast<float*>(lds + kSelectScratch);
+    const int S = keys_of(p, b);
+    const float* src = scores + k_begin(p, b);
+    constexpr int U = 8;
+    for (int i0 = threadIdx.x; i0 < S; i0 += U * kSelThreads) {
+        float v[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * kSelThreads;
+            v[u] = i < S ? ld<true>(src + i) : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * kSelThreads;
+            if (i < S) sl[i] = v[u];
+        }
+    }
+    __syncthreads();
+    const float t = f.lambda * reference_of<kSelThreads>(sl, p.R, S - p.R, f.reduce, red);
     if (threadIdx.x == 0) {
         if (f.tau) f.tau[b] = t;
         *tau_s = t;
     }
     __syncthreads();
-    compact_sample<kSelThreads, true>(p, scores, b, *tau_s, f.slot, f.count, wsum);
+    compact_of<kSelThreads>(sl + p.R, S - p.R, *tau_s, f.slot + cand_begin(p, b), f.count + b,
+                            wsum);
 }
 
 // ---------------------------------------------------------------------------

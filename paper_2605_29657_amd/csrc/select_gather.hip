@@ -12,11 +12,12 @@
 //              strip writes its survivors' candidate-local indices, ascending,
 //              to the sample's slot of the workspace (slot[co_b + i]).
 //              Optionally computes tau first (fused threshold of occam_prune).
-// pack_gather  grid (G, sample): every workgroup forms its sample's packed
-//              offset (exclusive sum of the counts before it), writes the
-//              packed survivor list (through index_map when given) and
-//              kept_offsets, and its waves copy survivor rows of every row
-//              tensor with 16-byte vector loads and stores.
+// pack_gather  grid (G, sample): every wave forms its sample's packed offset
+//              (exclusive sum of the counts before it, with shuffles: no
+//              barrier); the workgroups write the packed survivor list (through
+//              index_map when given) and kept_offsets, and their waves copy
+//              survivor rows of every row tensor with 16-byte vector loads and
+//              stores, one row per wave at a time.
 #include "occam_internal.hpp"
 
 namespace occam {
@@ -67,7 +68,6 @@ __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
     const int* __restrict__ index_map, int* __restrict__ kept_idx, int* __restrict__ kept_offsets,
     const int* __restrict__ packed_idx, const int* __restrict__ packed_offsets, RowTensors rows)
 {
-    __shared__ int red[kGatherThreads];
     const int b = blockIdx.y, x = blockIdx.x, G = gridDim.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int co = cand_begin(p, b);
@@ -78,15 +78,13 @@ __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
         cnt = packed_offsets[b + 1] - off;
         idx = packed_idx + off;
     } else {
+        // The sample's packed offset, the sum of the counts before it: every wave forms it
+        // on its own (strided partial sums, then a shuffle tree), so no barrier is needed.
         int acc = 0;
-        for (int j = tid; j < b; j += kGatherThreads) acc += count[j];
-        red[tid] = acc;
-        __syncthreads();
-        for (int s = kGatherThreads / 2; s > 0; s >>= 1) {
-            if (tid < s) red[tid] += red[tid + s];
-            __syncthreads();
-        }
-        off = red[0];
+        for (int j = lane; j < b; j += kWave) acc += count[j];
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+        off = acc;
         cnt = count[b];
         idx = slot + co;
         if (x == 0 && tid == 0) {

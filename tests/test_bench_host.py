@@ -99,7 +99,7 @@ def test_trace_summary_finds_the_step_sequence_and_the_lone_scoring_loop(tmp_pat
         w.writeheader()
         w.writerows(rows)
     got = bench.trace_summary(str(path), warmup=5, steps=20)
-    assert [x["avg_us"] for x in got["steps"]] == [10.0 * (k + 1) + 1.0 for k in range(8)]
+    assert [x["avg_us"] for x in got["steps"]] == [10.0 * (k + 1) + 1.0 for k in range(len(names))]
     assert got["text_score_alone"]["n"] == 20
     assert got["text_score_alone"]["min_us"] == 201.0 and got["text_score_alone"]["max_us"] == 220.0
 

@@ -103,6 +103,78 @@ def test_headline_full_batch_sampled(stage):
     check_rows(g, sb)
 
 
+def replicate(one: synth.StageBatch, n: int) -> synth.StageBatch:
+    """A batch of n copies of a one-sample batch (same shapes, offsets of a batch of n)."""
+    assert one.B == 1
+    T, N = np.repeat(one.T, n), np.repeat(one.N, n)
+    sb = synth.StageBatch(workload=one.workload, stage=one.stage, dtype=one.dtype, B=n, R=one.R,
+                          H=one.H, Hkv=one.Hkv, d=one.d, T=T, N=N,
+                          q_off=np.concatenate([[0], np.cumsum(T)]).astype(np.int64),
+                          k_off=np.concatenate([[0], np.cumsum(N + one.R)]).astype(np.int64),
+                          q=np.concatenate([one.q] * n, axis=0), k=np.concatenate([one.k] * n, axis=0))
+    for pl in one.payload:
+        rows = sb.k.reshape(sb.k.shape[0], -1) if pl.name == "k_rows" else np.concatenate([pl.rows] * n, 0)
+        sb.payload.append(synth.Payload(pl.name, rows, pl.pad_rows, pl.row0))
+    return sb
+
+
+def full_batch_sampled(name, stage, pick, ragged, sb=None, sub=None, oracle_of=None):
+    """The whole batch in the benchmark's launch configuration; the picked samples are
+    recomputed by the oracle (sample pick[j] against oracle sample oracle_of[j] of `sub`),
+    every sample's bookkeeping and rows are checked."""
+    lam = lam_for(name, stage)
+    sb = synth.make_stage(name, stage) if sb is None else sb
+    print("case: full batch %s/%s B=%d ragged=%s oracle samples %s" % (name, stage, sb.B, ragged,
+                                                                       pick), flush=True)
+    ds = DeviceStage(sb, ragged=ragged)
+    ds.prune(lam)
+    g = ds.host()
+    sub = synth.make_stage(name, stage, samples=pick) if sub is None else sub
+    oracle_of = list(range(len(pick))) if oracle_of is None else oracle_of
+    o = oracle_prune(sub, lam)
+    rtol = RTOL[sb.dtype]
+    worst = 0.0
+    for b, j in zip(pick, oracle_of):
+        gs = g["scores"][sb.k_off[b]:sb.k_off[b + 1]]
+        worst = max(worst, check_scores(gs, o["scores"][sub.k_off[j]:sub.k_off[j + 1]], rtol))
+        check_scores(g["tau"][b:b + 1], o["tau"][j:j + 1], rtol, "tau")
+        gsel = dict(kept_idx=g["kept_idx"][g["kept_offsets"][b]:g["kept_offsets"][b + 1]],
+                    kept_count=g["kept_count"][b:b + 1],
+                    kept_offsets=np.array([0, g["kept_count"][b]]))
+        one = synth.StageBatch(workload=name, stage=stage, dtype=sb.dtype, B=1, R=sb.R, H=sb.H,
+                               Hkv=sb.Hkv, d=sb.d, T=sb.T[b:b + 1], N=sb.N[b:b + 1],
+                               q_off=np.array([0, sb.T[b]]), k_off=np.array([0, sb.N[b] + sb.R]),
+                               q=None, k=None)
+        oj = dict(scores=o["scores"][sub.k_off[j]:sub.k_off[j + 1]], tau=o["tau"][j:j + 1],
+                  kept_idx=o["kept_idx"][o["kept_offsets"][j]:o["kept_offsets"][j + 1]],
+                  kept_offsets=np.array([0, o["kept_count"][j]]))
+        check_selection(gsel, oj, one, rtol)
+    check_bookkeeping(g, sb)
+    check_rows(g, sb)
+    print("  max rel score err %.3g over samples %s" % (worst, pick), flush=True)
+
+
+@pytest.mark.parametrize("stage", ["vis", "txt"])
+def test_qwen3vl_full_batch_sampled(stage):
+    # B = 64 ragged, as the benchmark launches it; the oracle recomputes the first and last
+    # samples and sample 13, which has 512 text rows (four row blocks).
+    sb = synth.make_stage("qwen3vl_ragged", stage)
+    if stage == "txt":
+        assert sb.T[13] == 512
+    full_batch_sampled("qwen3vl_ragged", stage, [0, 13, 63], ragged=True, sb=sb)
+
+
+@pytest.mark.parametrize("stage", ["vis", "txt"])
+def test_video_full_batch_sampled(stage):
+    # B = 8 uniform at full size (16384 visual tokens and 8 registers per sample; 256 text
+    # rows = two row blocks), launched as the benchmark launches it.  Every slot holds the
+    # bytes of sample 7 (drawing all eight samples takes minutes on the host), so the
+    # oracle's one result must be reproduced by every sample, at every base offset.
+    one = synth.make_stage("video", stage, samples=[7])
+    full_batch_sampled("video", stage, list(range(8)), ragged=False, sb=replicate(one, 8),
+                       sub=one, oracle_of=[0] * 8)
+
+
 # ----------------------------------------------------------------------------- mutual scoring
 # Stage I without a CLS row (Eq. mutual_scoring): every register and visual token is
 # an anchor row and each key is scored by the mean attention it receives.
