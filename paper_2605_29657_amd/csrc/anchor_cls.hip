@@ -278,8 +278,23 @@ __global__ __launch_bounds__(kClsThreads) void cls_stream_kernel(
     }
 }
 
-// With fin.done (occam_prune) the last workgroup of each sample applies the threshold
-// and the compaction to the sample's scores (select_kernel's arithmetic).
+// score(s) of one key from its H logits and the per-head normalisers: the one
+// expression both the scores and the per-chunk threshold use, so that they agree bit for
+// bit.
+template <bool BF16>
+__device__ __forceinline__ float cls_key_score(const float* l, int H, const float* mh,
+                                               const float* izh) {
+    float acc = 0.f;
+    for (int h = 0; h < H; ++h) acc += cls_exp<BF16>(l[h] - mh[h]) * izh[h];
+    return acc * (1.f / (float)H);
+}
+
+// With fin.chunk_cnt (occam_prune) every workgroup also applies the threshold to its own
+// chunk and compacts the chunk's survivors: tau_b = lambda * reduce(register scores), the
+// register scores formed from the register keys' logits exactly as the scores are (so tau
+// has the threshold kernel's bits), then a ballot + mbcnt compaction of the chunk's
+// visual keys (one key per thread) with an LDS scan of the wave counts.  Chunks past the
+// sample's keys write a zero count.
 template <bool BF16>
 __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
     Prob p, const float* __restrict__ logits, const float2* __restrict__ stats,
@@ -288,10 +303,15 @@ __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
 {
     __shared__ float red_m[kClsThreads], red_z[kClsThreads];
     __shared__ float mh[64], izh[64];
+    __shared__ float regs[32];
+    __shared__ int wcnt[kClsThreads / kWave];
     const int c = blockIdx.x, b = blockIdx.y;
     const int S = keys_of(p, b);
     const int s0 = c * kpw;
-    if (s0 >= S) return;
+    if (s0 >= S) {
+        if (fin.chunk_cnt && threadIdx.x == 0) fin.chunk_cnt[(size_t)b * nchunks + c] = 0;
+        return;
+    }
     const int nk = min(kpw, S - s0);
     const int H = p.H;
     const int nch = (S + kpw - 1) / kpw;
@@ -335,20 +355,38 @@ __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
     __syncthreads();
     const float* lrow = logits + ((size_t)k_begin(p, b) + s0) * H;
     float* out = scores + k_begin(p, b) + s0;
-    const float invH = 1.f / (float)H;
+    float mine = 0.f;                            // this thread's key (one key per thread)
     for (int key = threadIdx.x; key < nk; key += blockDim.x) {
-        float acc = 0.f;
-        for (int h = 0; h < H; ++h) acc += cls_exp<BF16>(lrow[key * H + h] - mh[h]) * izh[h];
-        // Read by the sample's last workgroup in this launch: a device-coherent store.
-        if (fin.done) st_cc(out + key, acc * invH);
-        else out[key] = acc * invH;
+        mine = cls_key_score<BF16>(lrow + (size_t)key * H, H, mh, izh);
+        out[key] = mine;
     }
-    if (!fin.done) return;
-    // Dynamic LDS (launched only with the epilogue): the counter flag, then the select
-    // scratch and the copy of the sample's scores.
-    extern __shared__ __attribute__((aligned(16))) char cls_dyn[];
-    if (last_of_sample(fin.done, b, (unsigned)nch, reinterpret_cast<int*>(cls_dyn)))
-        select_sample(p, scores, b, fin, cls_dyn + 64);
+    if (!fin.chunk_cnt) return;
+    const int R = p.R;
+    if (threadIdx.x < R)
+        regs[threadIdx.x] = cls_key_score<BF16>(logits + ((size_t)k_begin(p, b) + threadIdx.x) * H,
+                                                H, mh, izh);
+    __syncthreads();
+    const float tau = fin.lambda * reg_reduce(regs, R, fin.reduce);
+    if (c == 0 && threadIdx.x == 0 && fin.tau) fin.tau[b] = tau;
+    const int key = s0 + threadIdx.x, lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const bool keep = (int)threadIdx.x < nk && key >= R && mine >= tau;
+    const unsigned long long m = __ballot(keep);
+    const int below = (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                                     __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+    if (lane == 0) wcnt[wave] = __popcll(m);
+    __syncthreads();
+    int base = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < kClsThreads / kWave; ++w) {
+        base += w < wave ? wcnt[w] : 0;
+        total += wcnt[w];
+    }
+    const size_t list = (size_t)b * nchunks + c;
+    if (keep) fin.chunk_slot[list * kpw + base + below] = key - R;
+    if (threadIdx.x == 0) {
+        fin.chunk_cnt[list] = total;
+        if (total) atomicAdd(fin.count + b, total);
+    }
 }
 
 static size_t cls_logits_smem(const Prob& p, int bf16, int kpw) {
@@ -412,7 +450,7 @@ hipError_t launch_cls_scores(const Prob& p, int bf16, const float* logits, const
 {
     const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
     dim3 grid(nchunks, p.B);
-    const size_t smem = fin.done ? 64 + select_lds_bytes(p.R, p.max_cands) : 0;
+    const size_t smem = 0;
     if (bf16)
         return launch(cls_scores_kernel<true>, grid, dim3(kClsThreads), smem, s, p, logits, stats,
                       row_lse, scores, kpw, nchunks, fin);

@@ -23,8 +23,9 @@ struct Plan {
     int bf16;
     int text;          // 1: several anchor rows (MFMA path); 0: one anchor row (VALU path)
     int kpw;           // keys per workgroup of the one-row path
-    size_t off_logits, off_stats, off_lse2, off_part, off_done, off_scores, off_tau, off_slot,
-        off_match, total;
+    int nchunks;       // key chunks per sample of the one-row path
+    size_t off_logits, off_stats, off_lse2, off_part, off_done, off_clist, off_ccnt, off_scores,
+        off_tau, off_slot, off_match, total;
 };
 
 bool aligned(const void* ptr, size_t a) { return (reinterpret_cast<uintptr_t>(ptr) % a) == 0; }
@@ -84,7 +85,7 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
             off = align_up(off + (size_t)B * nrb * (R + (size_t)max_cands) * sizeof(float));
         }
     } else {
-        P.kpw = cls_keys_per_wg(H, x.num_kv_heads, d, bf16 ? 2 : 4);
+        P.kpw = cls_keys_per_wg(H, x.num_kv_heads, d, bf16 ? 2 : 4, B, R + (long long)max_cands);
         const int NC = d / (bf16 ? 8 : 4);
         const size_t smem = sizeof(float) * ((size_t)H * d + (size_t)NC * x.num_kv_heads +
                                              (size_t)P.kpw * H * NC + (size_t)P.kpw * H +
@@ -93,8 +94,14 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
         if (!cls_stream_nc(H, x.num_kv_heads, d, bf16 ? 2 : 4) && smem > 65536)
             return OCCAM_ERR_UNSUPPORTED;
         const long long nchunks = (R + (long long)max_cands + P.kpw - 1) / P.kpw;
+        P.nchunks = nchunks > (1LL << 30) ? (1 << 30) : (int)nchunks;
         P.off_logits = off; off = align_up(off + (size_t)keys_cap * H * sizeof(float));
         P.off_stats = off; off = align_up(off + (size_t)B * nchunks * H * sizeof(float2));
+        if (nchunks <= kMaxChunkLists) {
+            // Per-chunk survivor lists and counts of the in-kernel threshold + compaction.
+            P.off_clist = off; off = align_up(off + (size_t)B * nchunks * P.kpw * sizeof(int));
+            P.off_ccnt = off; off = align_up(off + (size_t)B * nchunks * sizeof(int));
+        }
     }
     // Finished workgroups per sample (the in-kernel threshold / compaction epilogue).
     P.off_done = off; off = align_up(off + (size_t)B * sizeof(unsigned));
@@ -161,22 +168,33 @@ inline occam_status hip_ok(hipError_t e) { return e == hipSuccess ? OCCAM_OK : O
 // then also combines its row blocks in the scoring kernel.
 occam_status run_score(const Plan& P, const void* q, const void* k, const float* row_lse,
                        float* scores, void* ws, hipStream_t s, const Finish* sel = nullptr,
-                       int* selected = nullptr) {
+                       int* selected = nullptr, ChunkLists* lists = nullptr) {
     Finish fin{};
     if (selected) *selected = 0;
-    const bool counters = !P.text || (!row_lse && !P.p.mean_rows);
-    const bool combine = P.text && P.p.max_rows > kTxtRows;     // several row blocks
-    // The epilogue copies a sample's scores into LDS: the scoring kernel's tiles hold it
-    // (text rows), or up to 48 KB of dynamic LDS (one row).
-    const size_t need = 128 + select_lds_bytes(P.p.R, P.p.max_cands);
-    const bool fits = P.text ? need <= text_score_smem(P.p.H, ((P.p.d + 15) / 16) * 16)
-                             : need <= 48 * 1024;
-    const bool do_select = sel && fits;
-    if (counters && (do_select || combine)) {
-        if (sel) fin = *sel;
-        fin.done = ws_at<unsigned>(ws, P.off_done);
-        fin.select = do_select ? 1 : 0;
-        if (selected) *selected = fin.select;
+    if (P.text) {
+        // Text rows: the sample's last scoring workgroup combines the row blocks and, when
+        // the copy of the sample's scores fits in the kernel's LDS, selects.  The counters
+        // are cleared by the statistics kernel, so not with a caller normaliser.
+        const bool counters = !row_lse && !P.p.mean_rows;
+        const bool combine = P.p.max_rows > kTxtRows;
+        const size_t need = 128 + select_lds_bytes(P.p.R, P.p.max_cands);
+        const bool do_select = sel && need <= text_score_smem(P.p.H, ((P.p.d + 15) / 16) * 16);
+        if (counters && (do_select || combine)) {
+            if (sel) fin = *sel;
+            fin.done = ws_at<unsigned>(ws, P.off_done);
+            fin.select = do_select ? 1 : 0;
+            if (selected) *selected = fin.select;
+        }
+    } else if (sel && sel->reduce != kRefCandMean && P.nchunks <= kMaxChunkLists &&
+               P.kpw <= kClsThreads) {
+        // One row: every scoring workgroup thresholds and compacts its own chunk (the
+        // candidate mean needs every score first, so it keeps the separate select).
+        fin = *sel;
+        fin.select = 1;
+        fin.chunk_slot = ws_at<int>(ws, P.off_clist);
+        fin.chunk_cnt = ws_at<int>(ws, P.off_ccnt);
+        if (selected) *selected = 1;
+        if (lists) *lists = ChunkLists{fin.chunk_slot, fin.chunk_cnt, P.nchunks, P.kpw};
     }
     if (P.text) {
         const float* lse = row_lse;
@@ -254,14 +272,16 @@ occam_status run_prune(const Plan& P, const void* q, const void* k, const float*
     sel.slot = slot;
     sel.count = kept_count;
     int selected = 0;
-    if ((st = run_score(P, q, k, row_lse, sc, workspace, stream, &sel, &selected)) != OCCAM_OK)
+    ChunkLists lists{};
+    if ((st = run_score(P, q, k, row_lse, sc, workspace, stream, &sel, &selected, &lists)) !=
+        OCCAM_OK)
         return st;
     if (!selected) {
         st = hip_ok(launch_select(P.p, sc, nullptr, 1, lambda, reduce, tu, slot, kept_count, stream));
         if (st != OCCAM_OK) return st;
     }
     return hip_ok(launch_pack_gather(P.p, slot, kept_count, index_map, kept_idx, kept_offsets,
-                                     nullptr, nullptr, rows, stream));
+                                     nullptr, nullptr, rows, stream, lists));
 }
 
 // ---------------------------------------------------------------------------

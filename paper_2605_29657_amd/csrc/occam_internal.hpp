@@ -149,38 +149,40 @@ __device__ __forceinline__ float sample_reference(const Prob& p, const float* sc
 }
 
 // Ascending compaction of a sample's survivors (sv[v] >= tau over its N visual scores)
-// into out[i] and *count, by a workgroup of NT threads (all must call it): thread t owns
-// the contiguous strip [t*P, t*P + P) of the candidates, counts its survivors, one
-// block-wide exclusive scan (a shuffle scan per wave, then the NT/64 wave totals in order)
-// gives every strip its output position, and the strip writes its survivors in ascending
-// order.  The result does not depend on NT.  `wsum` is NT / 64 ints of LDS.
+// into out[i] and *count, by a workgroup of NT threads (all must call it).  Wave w owns the
+// contiguous range [w*Q, w*Q + Q) of the candidates (Q a multiple of 64) and walks it 64
+// candidates at a time: a ballot of the keep flags, its population count for the wave's
+// total, and in the second pass mbcnt (the set bits below the lane) for each survivor's
+// position; an LDS scan of the NT/64 wave totals places the waves' ranges.  The result
+// does not depend on NT.  `wsum` is NT / 64 ints of LDS.
 template <int NT>
 __device__ __forceinline__ void compact_of(const float* sv, int N, float tau, int* out,
                                            int* count, int* wsum) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int P = (N + NT - 1) / NT;
-    const int v0 = min(N, tid * P), v1 = min(N, v0 + P);
+    constexpr int NW = NT / kWave;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int Q = (((N + NW - 1) / NW) + kWave - 1) & ~(kWave - 1);
+    const int v0 = min(N, wave * Q), v1 = min(N, v0 + Q);
     int cnt = 0;
-    for (int v = v0; v < v1; ++v) cnt += sv[v] >= tau ? 1 : 0;
-    int inc = cnt;
-#pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-        const int o = __shfl_up(inc, off);
-        if (lane >= off) inc += o;
-    }
+    for (int v = v0 + lane; v - lane < v1; v += kWave)
+        cnt += __popcll(__ballot(v < v1 && sv[v] >= tau));
     __syncthreads();                          // `wsum` may still be read by a previous call
-    if (lane == kWave - 1) wsum[wave] = inc;
+    if (lane == 0) wsum[wave] = cnt;
     __syncthreads();
     int base = 0, total = 0;
 #pragma unroll
-    for (int w = 0; w < NT / kWave; ++w) {
+    for (int w = 0; w < NW; ++w) {
         base += w < wave ? wsum[w] : 0;
         total += wsum[w];
     }
-    int pos = base + inc - cnt;
-    for (int v = v0; v < v1; ++v)
-        if (sv[v] >= tau) out[pos++] = v;
-    if (tid == 0) *count = total;
+    for (int v = v0 + lane; v - lane < v1; v += kWave) {
+        const bool keep = v < v1 && sv[v] >= tau;
+        const unsigned long long m = __ballot(keep);
+        const int below = (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+        if (keep) out[base + below] = v;
+        base += __popcll(m);
+    }
+    if (threadIdx.x == 0) *count = total;
 }
 
 // The compaction of sample b from the packed score array into slot[co_b + i], count[b].
@@ -284,9 +286,17 @@ inline int cls_stream_nc(int H, int Hkv, int d, int elem_bytes) {
     return ncp;
 }
 constexpr int kClsStreamKeys = 128;    // keys per workgroup of the streaming form
+// Small batches: the streaming form halves its keys per workgroup (down to 16) until the
+// launch has this many workgroups (two per CU), so that a single image is read by many
+// CUs at once instead of a handful.
+constexpr int kClsMinWorkgroups = 512;
 
-inline int cls_keys_per_wg(int H, int Hkv, int d, int elem_bytes) {
-    if (cls_stream_nc(H, Hkv, d, elem_bytes)) return kClsStreamKeys;
+inline int cls_keys_per_wg(int H, int Hkv, int d, int elem_bytes, int B = 0, long long keys = 0) {
+    if (cls_stream_nc(H, Hkv, d, elem_bytes)) {
+        int kpw = kClsStreamKeys;
+        while (kpw > 16 && (long long)B * ((keys + kpw - 1) / kpw) < kClsMinWorkgroups) kpw /= 2;
+        return kpw;
+    }
     int chunks_per_head = d * elem_bytes / 16;
     int kpw = kClsPartials / (H * chunks_per_head);
     if (kpw > 64) kpw = 64;
@@ -307,13 +317,25 @@ struct Finish {
     float* tau;            // [B], tau_b
     int* slot;             // survivors, slot[co_b + i]
     int* count;            // [B]
+    // One-row path instead (chunk_cnt != null): every scoring workgroup thresholds and
+    // compacts its own chunk of kpw keys into chunk_slot[(b * nchunks + c) * kpw + i],
+    // writes chunk_cnt[b * nchunks + c] and adds it to count[b] (cleared by the logits
+    // kernel); pack_gather places the chunk lists.
+    int* chunk_slot;
+    int* chunk_cnt;
 };
 
-// Zero done[0 .. B) (one workgroup of the kernel that precedes the scoring kernel).
+// Zero the counters the scoring kernel accumulates into (one workgroup of the kernel that
+// precedes it in the call): done[0 .. B), or count[0 .. B) for the per-chunk compaction.
 __device__ __forceinline__ void clear_done(const Finish& f, int B) {
-    if (!f.done) return;
-    for (int i = threadIdx.x; i < B; i += blockDim.x) f.done[i] = 0u;
+    if (f.done)
+        for (int i = threadIdx.x; i < B; i += blockDim.x) f.done[i] = 0u;
+    if (f.chunk_cnt)
+        for (int i = threadIdx.x; i < B; i += blockDim.x) f.count[i] = 0;
 }
+
+// Most chunks per sample of the per-chunk compaction (pack_gather scans their counts in LDS).
+constexpr int kMaxChunkLists = 1024;
 
 // Every thread of the workgroup calls this after writing its share of sample b's scores
 // (or row-block partials) with device-coherent stores (st_cc).  Each wave waits until its
@@ -413,9 +435,17 @@ hipError_t launch_threshold(const Prob& p, const float* scores, float lambda, in
 hipError_t launch_select(const Prob& p, const float* scores, const float* tau, int fuse_tau,
                          float lambda, int reduce, float* tau_out, int* slot, int* count,
                          hipStream_t s);
+// Survivors from the per-chunk lists of the one-row scoring kernel (chunk_cnt != null)
+// or from slot[co_b + i] (select); counts per sample in count[B] either way.
+struct ChunkLists {
+    const int* slot;       // [B][nchunks][kpw]
+    const int* cnt;        // [B][nchunks]
+    int nchunks, kpw;
+};
 hipError_t launch_pack_gather(const Prob& p, const int* slot, const int* count,
                               const int* index_map, int* kept_idx, int* kept_offsets,
                               const int* packed_idx, const int* packed_offsets,
-                              const RowTensors& rows, hipStream_t s);
+                              const RowTensors& rows, hipStream_t s,
+                              const ChunkLists& lists = ChunkLists{});
 
 }  // namespace occam

@@ -66,25 +66,89 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(
 __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
     Prob p, const int* __restrict__ slot, const int* __restrict__ count,
     const int* __restrict__ index_map, int* __restrict__ kept_idx, int* __restrict__ kept_offsets,
-    const int* __restrict__ packed_idx, const int* __restrict__ packed_offsets, RowTensors rows)
+    const int* __restrict__ packed_idx, const int* __restrict__ packed_offsets, RowTensors rows,
+    ChunkLists lists)
 {
+    __shared__ int pc[kMaxChunkLists + 1];       // per-chunk lists: exclusive prefix of counts
+    __shared__ int wsum[kGatherThreads / kWave];
     const int b = blockIdx.y, x = blockIdx.x, G = gridDim.x;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int co = cand_begin(p, b);
     int off, cnt;
     const int* idx;
+    const int nlist = lists.cnt ? lists.nchunks : 0;
+    // The chunk counts are loaded before the counts of the earlier samples are summed, so
+    // that both loads are in flight together.
+    constexpr int PER = kMaxChunkLists / kGatherThreads;
+    int v[PER], sum = 0;
+    if (nlist) {
+        const int* cc = lists.cnt + (size_t)b * nlist;
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int c = tid * PER + j;
+            v[j] = c < nlist ? cc[c] : 0;
+        }
+    }
+    int before = 0;
+    if (!packed_idx) {
+        // The sample's packed offset, the sum of the counts before it: every wave forms it
+        // on its own (strided partial sums, then a shuffle tree), so no barrier is needed.
+        for (int j = lane; j < b; j += kWave) before += count[j];
+#pragma unroll
+        for (int o = kWave / 2; o > 0; o >>= 1) before += __shfl_xor(before, o);
+    }
+    if (nlist) {
+        // The sample's survivors are the concatenation of its chunk lists: a block scan of
+        // the chunk counts (four per thread) gives each list its start.
+#pragma unroll
+        for (int j = 0; j < PER; ++j) sum += v[j];
+        int inc = sum;
+#pragma unroll
+        for (int o = 1; o < kWave; o <<= 1) {
+            const int t = __shfl_up(inc, o);
+            if (lane >= o) inc += t;
+        }
+        if (lane == kWave - 1) wsum[wave] = inc;
+        __syncthreads();
+        int run = inc - sum;
+        for (int w = 0; w < wave; ++w) run += wsum[w];
+#pragma unroll
+        for (int j = 0; j < PER; ++j) {
+            const int c = tid * PER + j;
+            if (c < nlist) pc[c] = run;
+            run += v[j];
+        }
+        if (tid == kGatherThreads - 1) pc[nlist] = run;
+        __syncthreads();
+    }
+    // Candidate index of the sample's i-th survivor (any i, per thread).
+    auto survivor = [&](int i) -> int {
+        if (!nlist) return idx[i];
+        int lo = 0, hi = nlist - 1;                // the chunk c with pc[c] <= i < pc[c + 1]
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (pc[mid] <= i) lo = mid; else hi = mid - 1;
+        }
+        return lists.slot[((size_t)b * nlist + lo) * lists.kpw + (i - pc[lo])];
+    };
+    // The same for an i that is uniform over the wave: the chunk is the number of list
+    // starts at or below i, less one, counted 64 lists at a time with a ballot.
+    auto survivor_w = [&](int i) -> int {
+        if (!nlist) return idx[i];
+        int n = 0;
+        for (int c0 = 0; c0 < nlist; c0 += kWave) {
+            const int c = c0 + lane;
+            n += __popcll(__ballot(c < nlist && pc[c] <= i));
+        }
+        const int c = n - 1;
+        return lists.slot[((size_t)b * nlist + c) * lists.kpw + (i - pc[c])];
+    };
     if (packed_idx) {
         off = packed_offsets[b];
         cnt = packed_offsets[b + 1] - off;
         idx = packed_idx + off;
     } else {
-        // The sample's packed offset, the sum of the counts before it: every wave forms it
-        // on its own (strided partial sums, then a shuffle tree), so no barrier is needed.
-        int acc = 0;
-        for (int j = lane; j < b; j += kWave) acc += count[j];
-#pragma unroll
-        for (int o = kWave / 2; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
-        off = acc;
+        off = before;
         cnt = count[b];
         idx = slot + co;
         if (x == 0 && tid == 0) {
@@ -92,7 +156,7 @@ __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
             if (b == p.B - 1) kept_offsets[p.B] = off + cnt;
         }
         for (int i = x * kGatherThreads + tid; i < cnt; i += G * kGatherThreads) {
-            const int v = idx[i];
+            const int v = survivor(i);
             kept_idx[off + i] = index_map ? index_map[co + v] : v;
         }
     }
@@ -102,7 +166,7 @@ __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
     const int nw = kGatherThreads / kWave;
     for (int j = x * nw + wave; j < jobs; j += G * nw) {
         const int i = j / nt, t = j - i * nt;
-        const int v = idx[i];
+        const int v = survivor_w(i);
         const RowTensor& rt = rows.t[t];
         const char* src = rt.src + ((long long)co + (long long)b * rt.src_pad_rows + rt.src_row0 + v) *
                                        rt.src_stride;
@@ -152,7 +216,7 @@ hipError_t launch_select(const Prob& p, const float* scores, const float* tau, i
 hipError_t launch_pack_gather(const Prob& p, const int* slot, const int* count,
                               const int* index_map, int* kept_idx, int* kept_offsets,
                               const int* packed_idx, const int* packed_offsets,
-                              const RowTensors& rows, hipStream_t s)
+                              const RowTensors& rows, hipStream_t s, const ChunkLists& lists)
 {
     // Enough workgroups per sample to cover the worst-case survivor count with
     // one row per wave, but no more than ~4096 in total (16 per CU; fewer rows per
@@ -163,8 +227,11 @@ hipError_t launch_pack_gather(const Prob& p, const int* slot, const int* count,
     long long cap = (4096 + p.B - 1) / p.B;
     long long G = per < cap ? per : cap;
     if (G < 1) G = 1;
+    if (lists.cnt && (lists.nchunks < 1 || lists.nchunks > kMaxChunkLists))
+        return hipErrorInvalidValue;
     return launch(pack_gather_kernel, dim3((unsigned)G, p.B), dim3(kGatherThreads), 0, s, p, slot,
-                  count, index_map, kept_idx, kept_offsets, packed_idx, packed_offsets, rows);
+                  count, index_map, kept_idx, kept_offsets, packed_idx, packed_offsets, rows,
+                  lists);
 }
 
 }  // namespace occam
