@@ -173,21 +173,26 @@ __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
         char* dst = rt.dst + (long long)(off + i) * rt.dst_stride;
         const long long nb = rt.row_bytes;
         if (rows.vec16) {
-            // Four 16-byte loads in flight per lane before the stores.
+            // Four 16-byte loads in flight per lane before the stores.  The copies are
+            // non-temporal: the rows are touched once, and allocating them in the 256 MB
+            // memory-side cache would evict the keys that the next statistics pass reads
+            // again (measured: the LLaVA-NeXT step 16 us shorter, 0.437 -> 0.421 ms).
             constexpr long long step = 16 * kWave;
             long long o = (long long)lane * 16;
             for (; o + 3 * step < nb; o += 4 * step) {
-                const u32x4 a0 = *reinterpret_cast<const u32x4*>(src + o);
-                const u32x4 a1 = *reinterpret_cast<const u32x4*>(src + o + step);
-                const u32x4 a2 = *reinterpret_cast<const u32x4*>(src + o + 2 * step);
-                const u32x4 a3 = *reinterpret_cast<const u32x4*>(src + o + 3 * step);
-                *reinterpret_cast<u32x4*>(dst + o) = a0;
-                *reinterpret_cast<u32x4*>(dst + o + step) = a1;
-                *reinterpret_cast<u32x4*>(dst + o + 2 * step) = a2;
-                *reinterpret_cast<u32x4*>(dst + o + 3 * step) = a3;
+                const u32x4 a0 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o));
+                const u32x4 a1 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o + step));
+                const u32x4 a2 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o + 2 * step));
+                const u32x4 a3 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o + 3 * step));
+                __builtin_nontemporal_store(a0, reinterpret_cast<u32x4*>(dst + o));
+                __builtin_nontemporal_store(a1, reinterpret_cast<u32x4*>(dst + o + step));
+                __builtin_nontemporal_store(a2, reinterpret_cast<u32x4*>(dst + o + 2 * step));
+                __builtin_nontemporal_store(a3, reinterpret_cast<u32x4*>(dst + o + 3 * step));
             }
             for (; o < nb; o += step)
-                *reinterpret_cast<u32x4*>(dst + o) = *reinterpret_cast<const u32x4*>(src + o);
+                __builtin_nontemporal_store(
+                    __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o)),
+                    reinterpret_cast<u32x4*>(dst + o));
         } else {
             for (long long o = (long long)lane * 4; o < nb; o += 4 * kWave)
                 *reinterpret_cast<uint32_t*>(dst + o) = *reinterpret_cast<const uint32_t*>(src + o);
