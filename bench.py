@@ -549,14 +549,15 @@ def traffic_from_counters(fetch_csv: str, write_csv: str, workload: str) -> dict
     fetch = f_kib * f_scale * 1024.0
     write = w_kib * w_scale * 1024.0
     extra = {}
-    try:
-        cf, _, n_c = read(fetch_csv, "cls_stream_kernel")
-        cw, _, _ = read(write_csv, "cls_stream_kernel")
-        extra = {"cls_stream": {"fetch_bytes": int(round(cf * f_scale * 1024.0)),
-                                "write_bytes": int(round(cw * w_scale * 1024.0)),
-                                "dispatches": n_c}}
-    except SystemExit:
-        pass
+    for key, kname in (("cls_stream", "cls_stream_kernel"), ("text_stats", "text_stats_kernel")):
+        try:
+            cf, _, n_c = read(fetch_csv, kname)
+            cw, _, _ = read(write_csv, kname)
+            extra[key] = {"fetch_bytes": int(round(cf * f_scale * 1024.0)),
+                          "write_bytes": int(round(cw * w_scale * 1024.0)),
+                          "dispatches": n_c}
+        except SystemExit:
+            pass
     return {**{"kernel": "text_score", "workload": workload,
             "bytes_per_launch": int(round(fetch + write)),
             "fetch_bytes": int(round(fetch)), "write_bytes": int(round(write)),
@@ -566,6 +567,35 @@ def traffic_from_counters(fetch_csv: str, write_csv: str, workload: str) -> dict
             "note": "FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of text_score, scaled by "
                     "what the same counters read for a 1 GiB device copy; see "
                     "text_score_traffic_llava_next.md"}, **extra}
+
+
+def fetch_summary(fetch_csv: str, write_csv: str) -> dict:
+    """Mean FETCH_SIZE and WRITE_SIZE per dispatch of every kernel in two rocprofv3 --pmc
+    runs of `bench.py --kernel-only`, in bytes, each scaled by what the same counter reads
+    for the run's last dispatch, the plain 1 GiB device copy."""
+    import csv
+    import re
+
+    def per_kernel(path):
+        rows = sorted(csv.DictReader(open(path)), key=lambda r: int(r["Dispatch_Id"]))
+        copy = [float(r["Counter_Value"]) for r in rows if "copyBuffer" in r["Kernel_Name"]]
+        if not copy:
+            raise SystemExit("%s: no calibration copy" % path)
+        scale = float(1 << 20) / copy[-1]
+        acc = {}
+        for r in rows:
+            name = re.sub(r"\(.*", "", r["Kernel_Name"]).replace("void ", "").replace("occam::", "")
+            if name.startswith(("at::", "__amd", "Cijk")):
+                continue
+            acc.setdefault(name, []).append(float(r["Counter_Value"]) * scale * 1024.0)
+        return {k: (sum(v) / len(v), len(v)) for k, v in acc.items()}, scale
+
+    f, fs = per_kernel(fetch_csv)
+    w, ws = per_kernel(write_csv)
+    return {"fetch_scale": round(fs, 4), "write_scale": round(ws, 4),
+            "kernels": {k: {"fetch_bytes": int(round(f[k][0])),
+                            "write_bytes": int(round(w.get(k, (0.0, 0))[0])),
+                            "dispatches": f[k][1]} for k in sorted(f)}}
 
 
 # Kernels of one headline step, in launch order: Stage I prune, then Stage II prune (three
@@ -582,10 +612,11 @@ STEP_KERNELS = [
 
 def trace_summary(trace_csv: str, warmup: int = 5, steps: int = 20) -> dict:
     """Per-kernel durations of the headline step from a rocprofv3 --kernel-trace CSV of
-    `bench.py --steps N`: the first warmup + steps occurrences of the step's kernel
-    sequence (other launches in between are skipped), timed steps only; and the scoring
-    kernel alone, the first `steps` of its launches after a warm-up that follow the
-    steps (the roofline measurement's loop)."""
+    `bench.py --steps N` (N = steps): the step's kernel sequence occurs in the settling,
+    warm-up and timed steps (at least warmup + steps times, no other measurement launches
+    it), and the timed steps are its last `steps` occurrences; then the scoring kernel
+    alone, the last `steps` launches of the run of lone scoring launches that follows (the
+    roofline measurement's loop)."""
     import csv
     import re
     import statistics as st
@@ -596,8 +627,8 @@ def trace_summary(trace_csv: str, warmup: int = 5, steps: int = 20) -> dict:
     dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
     names = [k for k, _ in STEP_KERNELS]
     ours = [i for i, n in enumerate(short) if not n.startswith(("at::", "__amd", "Cijk"))]
-    reps, j = [], 0
-    while j + len(names) <= len(ours) and len(reps) < warmup + steps:
+    reps, j, last = [], 0, -1
+    while j + len(names) <= len(ours):
         if [short[i] for i in ours[j:j + len(names)]] == names:
             reps.append([dur[i] for i in ours[j:j + len(names)]])
             last = ours[j + len(names) - 1]
@@ -606,13 +637,21 @@ def trace_summary(trace_csv: str, warmup: int = 5, steps: int = 20) -> dict:
             j += 1
     if len(reps) < warmup + steps:
         raise SystemExit("%s: found %d of %d steps" % (trace_csv, len(reps), warmup + steps))
-    timed = reps[warmup:]
+    timed = reps[-steps:]
     per = [{"kernel": label, "avg_us": round(st.mean(r[k] for r in timed), 1),
             "min_us": round(min(r[k] for r in timed), 1),
             "max_us": round(max(r[k] for r in timed), 1)} for k, (_, label) in enumerate(STEP_KERNELS)]
-    alone = [dur[i] for i, n in enumerate(short) if n == "text_score_kernel<8, false, true>" and i > last]
-    alone = alone[1:1 + steps]
+    lone = "text_score_kernel<8, false, true>"
+    after = [i for i in ours if i > last]
+    run = []
+    for i in after:
+        if short[i] == lone:
+            run.append(dur[i])
+        elif run:
+            break
+    alone = run[-steps:]
     return {"steps": per, "step_sum_us": round(sum(x["avg_us"] for x in per), 1),
+            "matched_steps": len(reps),
             "text_score_alone": {"n": len(alone), "avg_us": round(st.mean(alone), 1),
                                  "min_us": round(min(alone), 1), "max_us": round(max(alone), 1)}}
 
@@ -657,12 +696,18 @@ def main():
     ap.add_argument("--traffic-from", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
                     help="write profiles/traffic.json from the counter_collection.csv files "
                          "of two rocprofv3 --pmc runs (FETCH_SIZE, WRITE_SIZE) of --kernel-only")
+    ap.add_argument("--fetch-summary", nargs=2, metavar=("FETCH_CSV", "WRITE_CSV"),
+                    help="per-kernel FETCH_SIZE / WRITE_SIZE bytes (scaled by the calibration "
+                         "copy) from two rocprofv3 --pmc runs of --kernel-only")
     ap.add_argument("--trace-summary", metavar="TRACE_CSV",
                     help="per-kernel durations of the step from the kernel_trace.csv of a "
                          "rocprofv3 --kernel-trace run of `bench.py --steps K` (K = --steps)")
     args = ap.parse_args()
     if args.trace_summary:
         print(json.dumps(trace_summary(args.trace_summary, args.warmup, args.steps), indent=1))
+        return
+    if args.fetch_summary:
+        print(json.dumps(fetch_summary(*args.fetch_summary), indent=1))
         return
     if args.traffic_from:
         tj = traffic_from_counters(args.traffic_from[0], args.traffic_from[1], args.workload)
@@ -699,10 +744,13 @@ def main():
     if args.kernel_only:
         txt = synth.make_stage(name, "txt", payload=False)
         dt = DeviceStage(txt, ragged=txt.ragged, payload=False)
-        lse = reference_lse(torch, txt, dt)
         scores_buf = torch.empty_like(dt.out["scores"])
-        for _ in range(args.kernel_reps):
-            occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws, row_lse=lse)
+        if not txt.ragged:
+            # The scoring kernel alone needs a normaliser; the set-up computes it for a
+            # uniform batch only.
+            lse = reference_lse(torch, txt, dt)
+            for _ in range(args.kernel_reps):
+                occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws, row_lse=lse)
         for _ in range(args.kernel_reps):
             occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws)     # statistics + scoring
         # Stage I scoring (the one-row logits with online statistics, then the scores).

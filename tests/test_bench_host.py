@@ -86,13 +86,15 @@ def test_trace_summary_finds_the_step_sequence_and_the_lone_scoring_loop(tmp_pat
         t += int(us * 1000) + 500
 
     launch("at::native::fill", 3.0)                    # set-up work is skipped
-    for rep in range(25):                              # 5 warm-up + 20 timed steps
+    for rep in range(65):                              # 40 settling + 5 warm-up + 20 timed
         for k, n in enumerate(names):
-            launch(n, 10.0 * (k + 1) + (rep >= 5) * 1.0)
+            launch(n, 10.0 * (k + 1) + (rep >= 45) * 1.0)
         if rep == 7:
             launch("at::native::copy", 2.0)
-    for i in range(21):                                # one warm-up + 20 timed, alone
-        launch("text_score_kernel<8, false, true>", 200.0 + i)
+    for i in range(31):                                # settling + 20 timed, alone
+        launch("text_score_kernel<8, false, true>", 190.0 + i)
+    launch("text_stats_kernel<8, false, false, 4>", 150.0)   # the next measurement
+    launch("text_score_kernel<8, false, true>", 999.0)
     path = tmp_path / "trace.csv"
     with open(path, "w", newline="") as f:
         w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
@@ -100,8 +102,30 @@ def test_trace_summary_finds_the_step_sequence_and_the_lone_scoring_loop(tmp_pat
         w.writerows(rows)
     got = bench.trace_summary(str(path), warmup=5, steps=20)
     assert [x["avg_us"] for x in got["steps"]] == [10.0 * (k + 1) + 1.0 for k in range(len(names))]
+    assert got["matched_steps"] == 65
     assert got["text_score_alone"]["n"] == 20
     assert got["text_score_alone"]["min_us"] == 201.0 and got["text_score_alone"]["max_us"] == 220.0
+
+
+def test_fetch_summary_scales_every_kernel(tmp_path):
+    # Per-kernel means of FETCH_SIZE / WRITE_SIZE, scaled by the calibration copy (a 1 GiB
+    # copy whose FETCH_SIZE reads half its bytes); PyTorch's own kernels are skipped.
+    stats = "void occam::text_stats_kernel<8, false, false, 4>(occam::Prob, ...)"
+    score = "void occam::text_score_kernel<8, false, false>(occam::Prob, ...)"
+    copy = "__amd_rocclr_copyBuffer"
+    fetch, write = tmp_path / "f.csv", tmp_path / "w.csv"
+    _counter_csv(fetch, [("at::native::fill", "FETCH_SIZE", 5.0), (stats, "FETCH_SIZE", 100.0),
+                         (stats, "FETCH_SIZE", 300.0), (score, "FETCH_SIZE", 50.0),
+                         (copy, "FETCH_SIZE", 524288.0)])
+    _counter_csv(write, [(stats, "WRITE_SIZE", 4.0), (stats, "WRITE_SIZE", 6.0),
+                         (score, "WRITE_SIZE", 1.0), (copy, "WRITE_SIZE", 1048576.0)])
+    got = bench.fetch_summary(str(fetch), str(write))
+    assert got["fetch_scale"] == 2.0 and got["write_scale"] == 1.0
+    ks = got["kernels"]
+    assert set(ks) == {"text_stats_kernel<8, false, false, 4>", "text_score_kernel<8, false, false>"}
+    assert ks["text_stats_kernel<8, false, false, 4>"] == {"fetch_bytes": 200 * 2 * 1024,
+                                                           "write_bytes": 5 * 1024, "dispatches": 2}
+    assert ks["text_score_kernel<8, false, false>"]["fetch_bytes"] == 50 * 2 * 1024
 
 
 def test_step_description_covers_ragged_workloads():
