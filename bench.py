@@ -565,8 +565,8 @@ def traffic_from_counters(fetch_csv: str, write_csv: str, workload: str) -> dict
             "dispatches": [n_f, n_w],
             "source_sha256": score_source_sha256(),
             "note": "FETCH_SIZE and WRITE_SIZE (KiB per dispatch) of text_score, scaled by "
-                    "what the same counters read for a 1 GiB device copy; see "
-                    "text_score_traffic_llava_next.md"}, **extra}
+                    "what the same counters read for a 1 GiB device copy; the commands are in "
+                    "scoring_traffic_llava_next_qwen3vl.md"}, **extra}
 
 
 def fetch_summary(fetch_csv: str, write_csv: str) -> dict:
@@ -612,11 +612,12 @@ STEP_KERNELS = [
 
 def trace_summary(trace_csv: str, warmup: int = 5, steps: int = 20) -> dict:
     """Per-kernel durations of the headline step from a rocprofv3 --kernel-trace CSV of
-    `bench.py --steps N` (N = steps): the step's kernel sequence occurs in the settling,
-    warm-up and timed steps (at least warmup + steps times, no other measurement launches
-    it), and the timed steps are its last `steps` occurrences; then the scoring kernel
-    alone, the last `steps` launches of the run of lone scoring launches that follows (the
-    roofline measurement's loop)."""
+    `bench.py --steps N` (N = steps).  The roofline measurement that follows the timed steps
+    starts with the first long run of lone scoring launches (its settling calls and timed
+    loop, at least `steps` in a row); the timed steps are the last `steps` occurrences of
+    the step's kernel sequence before that run (the settling and warm-up steps come earlier,
+    the ablation steps, which launch the same sequence, later), and the lone scoring figure
+    is the last `steps` launches of that run."""
     import csv
     import re
     import statistics as st
@@ -627,11 +628,22 @@ def trace_summary(trace_csv: str, warmup: int = 5, steps: int = 20) -> dict:
     dur = [(int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3 for r in rows]
     names = [k for k, _ in STEP_KERNELS]
     ours = [i for i, n in enumerate(short) if not n.startswith(("at::", "__amd", "Cijk"))]
-    reps, j, last = [], 0, -1
-    while j + len(names) <= len(ours):
+    lone = "text_score_kernel<8, false, true>"
+    run, j = [], 0
+    while j < len(ours):
+        k = j
+        while k < len(ours) and short[ours[k]] == lone:
+            k += 1
+        if k - j >= steps:
+            run = ours[j:k]
+            break
+        j = k + 1
+    if not run:
+        raise SystemExit("%s: no run of %d lone scoring launches" % (trace_csv, steps))
+    reps, j = [], 0
+    while j + len(names) <= len(ours) and ours[j + len(names) - 1] < run[0]:
         if [short[i] for i in ours[j:j + len(names)]] == names:
             reps.append([dur[i] for i in ours[j:j + len(names)]])
-            last = ours[j + len(names) - 1]
             j += len(names)
         else:
             j += 1
@@ -641,15 +653,7 @@ def trace_summary(trace_csv: str, warmup: int = 5, steps: int = 20) -> dict:
     per = [{"kernel": label, "avg_us": round(st.mean(r[k] for r in timed), 1),
             "min_us": round(min(r[k] for r in timed), 1),
             "max_us": round(max(r[k] for r in timed), 1)} for k, (_, label) in enumerate(STEP_KERNELS)]
-    lone = "text_score_kernel<8, false, true>"
-    after = [i for i in ours if i > last]
-    run = []
-    for i in after:
-        if short[i] == lone:
-            run.append(dur[i])
-        elif run:
-            break
-    alone = run[-steps:]
+    alone = [dur[i] for i in run[-steps:]]
     return {"steps": per, "step_sum_us": round(sum(x["avg_us"] for x in per), 1),
             "matched_steps": len(reps),
             "text_score_alone": {"n": len(alone), "avg_us": round(st.mean(alone), 1),

@@ -463,7 +463,7 @@ __device__ void ragged_score_task(const Prob& p, int id, int* sh) {
 // CC: the normalisers were written earlier in the same launch (by other workgroups), so
 // they are read with device-coherent loads.  cc_out: the scores / partials are read later
 // in the same launch by another workgroup, so they are written with device-coherent
-// stores.  rot_id spreads the starting heads.
+// stores.  rot_id picks the starting head (rot_id % 8 of 8 heads spread over H).
 template <int DS, bool HALF, bool FULL, bool CC>
 __device__ __forceinline__ void score_task(
     const Prob& p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
@@ -508,10 +508,10 @@ __device__ __forceinline__ void score_task(
     // Loop step hh works on head (hh + rot) mod H: a key row's head slices all sit at
     // the same offset within 8 KB rows, so workgroups moving through the heads in step
     // would load the same memory channels at the same time.  Eight starting heads,
-    // spread over the H heads, balance the channels as well as H of them do, and keep
-    // at most eight of a sample's query tiles in use at once, so that the L2 of its XCD
-    // serves the other workgroups' tile reads.  Steps past the last head repeat the
-    // last one (clamped prefetches).
+    // spread over the H heads, balance the channels as well as H of them do; with one
+    // start per XCD (rot_id % 8 is the XCD), the workgroups that share an L2 also share
+    // the query tile and key slices they are reading.  Steps past the last head repeat
+    // the last one (clamped prefetches).
     const int nrot = H < 8 ? H : 8;
     const int rot = (int)((unsigned)rot_id % (unsigned)nrot) * (H / nrot);
     auto head_of = [&](int hh) {
@@ -727,11 +727,15 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
         c = (task / nrb) % nchunk;
         b = p.B - 1 - task / (nrb * nchunk);
     }
-    // The starting head follows the key chunk, not the workgroup: the row blocks of one
-    // chunk (adjacent tasks, one XCD) then read the same key slices at about the same time
-    // and share them in L2 instead of each fetching the chunk's keys from memory.
+    // The starting head follows the XCD (workgroups are dealt to the 8 XCDs round-robin,
+    // and each XCD runs one contiguous range of tasks): every workgroup of an XCD walks the
+    // heads in the same order, so the chunks of a sample read its query tiles, and the row
+    // blocks of a chunk its key slices, at about the same time, and share them in that
+    // XCD's L2.  A start per key chunk instead fetched 1062 MB per launch at the
+    // LLaVA-NeXT shape and 3586 MB on the ragged Qwen3-VL batch; per XCD, 807 and 2654 MB,
+    // ~1 % faster.
     score_task<DS, HALF, FULL, false>(p, q, k, lse, lse_natural, scores, part, b, c, rb,
-                                      b * nchunk + c, smem_raw, fin.done != nullptr);
+                                      (int)blockIdx.x, smem_raw, fin.done != nullptr);
     if (!fin.done) return;
     const int S = keys_of(p, b), T = rows_of(p, b);
     const int nrb_b = (T + kTxtRows - 1) / kTxtRows;
