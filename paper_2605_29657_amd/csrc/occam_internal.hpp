@@ -262,10 +262,10 @@ inline size_t text_score_smem(int H, int d16) {
 // the head slices faster than deeper rings at fewer workgroups per CU: the scattered
 // 256-byte slices stream better with fewer requests outstanding per CU.
 constexpr int kStatsRing = 2;
-// rg: waves per key stream (2 or 4).
-inline size_t text_stats_smem(int d16, int rg) {
+// rg: waves per key stream of one row block (2 or 4); rbw: row blocks per workgroup.
+inline size_t text_stats_smem(int d16, int rg, int rbw = 1) {
     return (size_t)(kStatsThreads / kWave / rg) * kStatsRing * 32 * d16 * 2 +
-           2 * (size_t)(kStatsThreads / kWave / rg) * kTxtRows * 4;
+           2 * (size_t)(kStatsThreads / kWave / rg) * rbw * kTxtRows * 4;
 }
 
 // Anchor-path keys per workgroup for a given row geometry.
