@@ -637,14 +637,11 @@ __device__ __forceinline__ void score_task(
                     for (int r = 0; r < 16; ++r)
                         abar[sp][r] += __builtin_amdgcn_exp2f(fmaf(acc[r], c2, -l2));
                 };
-                if constexpr (FULL) {
-                    // Every row block full (FULL: uniform T, a multiple of 128): the chain
-                    // of sub-block sp+1 is issued next to the exponentials of sub-block sp
-                    // (scheduling barriers keep each pair together), so the wave keeps the
-                    // matrix core and the vector unit busy at once; left to itself the
-                    // compiler issues all 32 MFMAs first.  With one workgroup per CU (few
-                    // keys per sample) this is 13 % faster.  A separate instantiation: the
-                    // two forms in one kernel need more registers and run slower.
+                // The chain of sub-block sp+1 is issued next to the exponentials of
+                // sub-block sp (scheduling barriers keep each pair together), so the wave
+                // keeps the matrix core and the vector unit busy at once; left to itself
+                // the compiler issues all 32 MFMAs first.
+                auto pipelined = [&]() {
                     f32x16 a0 = chain(0);
                     __builtin_amdgcn_sched_barrier(0);
                     f32x16 a1 = chain(1);
@@ -657,6 +654,17 @@ __device__ __forceinline__ void score_task(
                     soft(2, a0);
                     __builtin_amdgcn_sched_barrier(0);
                     soft(3, a1);
+                };
+                if constexpr (FULL) {
+                    // Every row block full (FULL: uniform T, a multiple of 128).  With one
+                    // workgroup per CU (few keys per sample) the pipelined order is 13 %
+                    // faster.  A separate instantiation: the two forms in one kernel need
+                    // more registers, and the uniform batches run slower with them.
+                    pipelined();
+                } else if (nsb == 4) {
+                    // A full row block of a ragged or partial batch takes the same order
+                    // (Qwen3-VL batch: ~1 % faster step).
+                    pipelined();
                 } else {
 #pragma unroll
                     for (int sp = 0; sp < 4; ++sp) {

@@ -177,22 +177,20 @@ __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
             // non-temporal: the rows are touched once, and allocating them in the 256 MB
             // memory-side cache would evict the keys that the next statistics pass reads
             // again (measured: the LLaVA-NeXT step 16 us shorter, 0.437 -> 0.421 ms).
+            // A 2 KB row (Stage I hidden states) is two loads per lane, both issued
+            // before either store.
             constexpr long long step = 16 * kWave;
-            long long o = (long long)lane * 16;
-            for (; o + 3 * step < nb; o += 4 * step) {
-                const u32x4 a0 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o));
-                const u32x4 a1 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o + step));
-                const u32x4 a2 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o + 2 * step));
-                const u32x4 a3 = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o + 3 * step));
-                __builtin_nontemporal_store(a0, reinterpret_cast<u32x4*>(dst + o));
-                __builtin_nontemporal_store(a1, reinterpret_cast<u32x4*>(dst + o + step));
-                __builtin_nontemporal_store(a2, reinterpret_cast<u32x4*>(dst + o + 2 * step));
-                __builtin_nontemporal_store(a3, reinterpret_cast<u32x4*>(dst + o + 3 * step));
+            for (long long o = (long long)lane * 16; o < nb; o += 4 * step) {
+                u32x4 a[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (o + u * step < nb)
+                        a[u] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o + u * step));
+#pragma unroll
+                for (int u = 0; u < 4; ++u)
+                    if (o + u * step < nb)
+                        __builtin_nontemporal_store(a[u], reinterpret_cast<u32x4*>(dst + o + u * step));
             }
-            for (; o < nb; o += step)
-                __builtin_nontemporal_store(
-                    __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src + o)),
-                    reinterpret_cast<u32x4*>(dst + o));
         } else {
             for (long long o = (long long)lane * 4; o < nb; o += 4 * kWave)
                 *reinterpret_cast<uint32_t*>(dst + o) = *reinterpret_cast<const uint32_t*>(src + o);
