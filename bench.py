@@ -460,7 +460,9 @@ def stage_breakdown(torch, dv, dt, txt, lam1: float, lam2: float, steps: int) ->
 def workload_step(torch, name: str, steps: int) -> dict:
     """The headline step (Stage I prune + Stage II prune over all tokens) on another
     workload shape: images/s, the step's algorithmic bytes over its time, and the text
-    stage's algorithmic MFMA rate (one Q K^T)."""
+    stage's algorithmic MFMA rate (one Q K^T) over the step; then the text stage alone
+    (its Q K^T rate, and with both passes' Q K^T), also for the samples with at least 312
+    text rows when the batch mixes row counts."""
     from paper_2605_29657_amd import synth
     from paper_2605_29657_amd.runner import DeviceStage
     with open(os.path.join(ROOT, "tests", "golden", "lambdas.json")) as f:
@@ -497,7 +499,30 @@ def workload_step(torch, name: str, steps: int) -> dict:
            "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
            "text_mfma_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
            "kept_stage1_mean": float(np.mean(kept1)), "kept_stage2_mean": float(np.mean(kept2))}
+
+    def text_stage(sb, ds):
+        fn = lambda: ds.prune(lam2)
+        settle(torch, fn)
+        e0.record()
+        for _ in range(steps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / steps
+        fl = float(np.sum(2.0 * sb.T.astype(np.float64) * (sb.N + sb.R) * sb.H * sb.d))
+        tf = fl / (t * 1e-3) / 1e12
+        return {"samples": int(sb.B), "ms": round(t, 4), "qk_tflops": round(tf, 1),
+                "mfma_frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
+                "two_pass_mfma_frac": round(2 * tf / MFMA_BF16_PEAK_TFLOPS, 4)}
+
+    out["text_stage"] = text_stage(txt, dt)
     del dv, dt
+    big = [b for b in range(txt.B) if txt.T[b] >= 312]
+    if big and len(big) < txt.B:
+        sub = synth.make_stage(name, "txt", samples=big)
+        ds = DeviceStage(sub, ragged=sub.ragged)
+        out["text_stage"]["t_ge_312"] = text_stage(sub, ds)
+        del ds
     torch.cuda.empty_cache()
     return out
 

@@ -256,7 +256,10 @@ occam_status occam_prune_noalloc(const occam_problem *problem, const void *q, co
  * scores: device f32 in the layout occam_score writes.  lambda, mean_kept
  * (nullable): one device f32 each; mean_kept[0] receives the matched mean count.
  * A batch without candidates gives lambda 1.  Ratios are formed in float32; every
- * s_b(r) must be positive.  k_target finite >= 0.  The selection state lives in the
+ * s_b(r) must be positive.  k_target finite >= 0.  The count is of visual
+ * survivors only: the R registers, which every sample keeps whatever lambda is
+ * (the union with {r} in Eqs. stage1 and stage2), are not counted, so a target
+ * that includes them is k_target + R.  The selection state lives in the
  * workspace of the problem and is cleared by each call, so calls that share a
  * workspace must be ordered on one stream. */
 occam_status occam_match_lambda(const occam_problem *problem, const float *scores,
