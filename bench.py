@@ -629,7 +629,7 @@ STEP_KERNELS = [
     ("cls_stream_kernel<true, 8, 2>", "cls_stream (Stage I logits + online statistics)"),
     ("cls_scores_kernel<true>", "cls_scores (Stage I scores, threshold, compaction)"),
     ("pack_gather_kernel", "pack_gather (Stage I: 1024-wide hidden rows)"),
-    ("text_stats_kernel<8, false, false, 4>", "text_stats (Stage II normalisers)"),
+    ("text_stats_kernel<8, false, false, 4, 1>", "text_stats (Stage II normalisers)"),
     ("text_score_kernel<8, false, true>", "text_score (Stage II scores, threshold, compaction)"),
     ("pack_gather_kernel", "pack_gather (Stage II: hidden, K and V rows)"),
 ]

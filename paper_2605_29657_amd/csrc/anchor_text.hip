@@ -12,7 +12,8 @@
 // Every (row, head) softmax needs its normaliser before the head mean can be
 // formed, so the path has two passes over the keys:
 //
-// text_stats  task (sample, head, group of 1, 2 or 4 row blocks of 128), XCD-aware.
+// text_stats  task (sample, head, group of 1, 2 or 4 row blocks of 128; groups only
+//             when a sample has at most four row blocks), XCD-aware.
 //             One key stream consumed by four waves of 32 rows per row block (the
 //             kernel also has a two-stream form of two 64-row waves each), so each
 //             key block is copied once for every row block of the group; the
@@ -832,13 +833,15 @@ template <int DS, bool HALF, bool COLSUM>
 static hipError_t stats_launch(const Prob& p, const void* q, const void* k, float* lse2,
                                const float* lse_in, int lse_natural, float* part,
                                const Finish& fin, hipStream_t s) {
-    // With several row blocks per sample, one workgroup takes two or four of them and
+    // With two to four row blocks per sample, one workgroup takes two or four of them and
     // copies each key block once for all: on the ragged Qwen3-VL batch (up to 4 row
     // blocks) the pass fetches 1403 MB, its algorithmic bytes, instead of 1965 MB with
-    // one row block per workgroup (1722 MB with two), ~1 % faster.
+    // one row block per workgroup (1722 MB with two), ~1 % faster.  Taller batches keep
+    // one row block per workgroup: the mutual-scoring Stage I of the same batch (up to 32
+    // row blocks) took 4.42 ms with four per workgroup, 3.84 ms with two, 3.83 ms with one.
     if constexpr (!COLSUM) {
         const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
-        if (nrb >= 3)
+        if (nrb == 3 || nrb == 4)
             return stats_launch_rg<DS, HALF, COLSUM, 4, 4>(p, q, k, lse2, lse_in, lse_natural, part,
                                                            fin, s);
         if (nrb == 2)

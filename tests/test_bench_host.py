@@ -93,8 +93,11 @@ def test_trace_summary_finds_the_step_sequence_and_the_lone_scoring_loop(tmp_pat
             launch("at::native::copy", 2.0)
     for i in range(31):                                # settling + 20 timed, alone
         launch("text_score_kernel<8, false, true>", 190.0 + i)
-    launch("text_stats_kernel<8, false, false, 4>", 150.0)   # the next measurement
+    launch("text_stats_kernel<8, false, false, 4, 1>", 150.0)   # the next measurement
     launch("text_score_kernel<8, false, true>", 999.0)
+    for rep in range(30):                              # ablation steps: the same sequence
+        for k, n in enumerate(names):
+            launch(n, 500.0)
     path = tmp_path / "trace.csv"
     with open(path, "w", newline="") as f:
         w = csv.DictWriter(f, fieldnames=["Kernel_Name", "Start_Timestamp", "End_Timestamp"])
@@ -110,7 +113,7 @@ def test_trace_summary_finds_the_step_sequence_and_the_lone_scoring_loop(tmp_pat
 def test_fetch_summary_scales_every_kernel(tmp_path):
     # Per-kernel means of FETCH_SIZE / WRITE_SIZE, scaled by the calibration copy (a 1 GiB
     # copy whose FETCH_SIZE reads half its bytes); PyTorch's own kernels are skipped.
-    stats = "void occam::text_stats_kernel<8, false, false, 4>(occam::Prob, ...)"
+    stats = "void occam::text_stats_kernel<8, false, false, 4, 1>(occam::Prob, ...)"
     score = "void occam::text_score_kernel<8, false, false>(occam::Prob, ...)"
     copy = "__amd_rocclr_copyBuffer"
     fetch, write = tmp_path / "f.csv", tmp_path / "w.csv"
@@ -122,8 +125,8 @@ def test_fetch_summary_scales_every_kernel(tmp_path):
     got = bench.fetch_summary(str(fetch), str(write))
     assert got["fetch_scale"] == 2.0 and got["write_scale"] == 1.0
     ks = got["kernels"]
-    assert set(ks) == {"text_stats_kernel<8, false, false, 4>", "text_score_kernel<8, false, false>"}
-    assert ks["text_stats_kernel<8, false, false, 4>"] == {"fetch_bytes": 200 * 2 * 1024,
+    assert set(ks) == {"text_stats_kernel<8, false, false, 4, 1>", "text_score_kernel<8, false, false>"}
+    assert ks["text_stats_kernel<8, false, false, 4, 1>"] == {"fetch_bytes": 200 * 2 * 1024,
                                                            "write_bytes": 5 * 1024, "dispatches": 2}
     assert ks["text_score_kernel<8, false, false>"]["fetch_bytes"] == 50 * 2 * 1024
 

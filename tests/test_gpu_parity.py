@@ -260,6 +260,17 @@ def test_ragged_text_with_empty_and_long_samples():
     run_and_check(sb, 1.5)
 
 
+def test_statistics_row_block_groups():
+    # Three and four 128-row blocks at most: the statistics pass takes four row blocks per
+    # workgroup, so a group holds row blocks past a sample's rows (idle waves that still copy
+    # their share of every key block).  d = 72 gives a key block of five copies for the 16
+    # waves of a group (some waves copy nothing).
+    for T, d in (([300, 50, 129, 1], 128), ([500, 257, 3], 72)):
+        sb = custom_stage(B=len(T), R=4, H=8, Hkv=8, d=d, T=T, N=[400, 90, 0, 33][:len(T)],
+                          seed=len(T))
+        run_and_check(sb, 1.2)
+
+
 def test_lambda_zero_keeps_everything_and_huge_keeps_nothing():
     sb = custom_stage(B=3, R=2, H=4, Hkv=2, d=64, T=[40] * 3, N=[100] * 3)
     g, _ = run_and_check(sb, 0.0)
