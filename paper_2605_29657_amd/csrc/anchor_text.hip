@@ -13,7 +13,9 @@
 // formed, so the path has two passes over the keys:
 //
 // text_stats  task (sample, head, group of 1, 2 or 4 row blocks of 128; groups only
-//             when a sample has at most four row blocks), XCD-aware.
+//             when a sample has at most four row blocks[, key range]), XCD-aware; a
+//             batch with few such tasks splits their keys into ranges whose tables
+//             text_lse_merge combines.
 //             One key stream consumed by four waves of 32 rows per row block (the
 //             kernel also has a two-stream form of two 64-row waves each), so each
 //             key block is copied once for every row block of the group; the
@@ -126,8 +128,10 @@ template <int DS, bool HALF, bool COLSUM, int RG, int RING, int RBW>
 __device__ __forceinline__ void stats_task(
     const Prob& p, const uint16_t* __restrict__ q, const uint16_t* __restrict__ k,
     float* __restrict__ lse2, const float* __restrict__ lse_in, int lse_natural,
-    float* __restrict__ part, int b, int h, int tblk, char* smem_raw)
+    float* __restrict__ part, int b, int h, int tblk, int split, int nsplit, char* smem_raw)
 {
+    // Keys: range split of nsplit (32-key blocks [kb_lo, kb_lo + nkb_s) of the sample);
+    // the base-2 log-sum-exp over that range goes to table split of lse2.
     // RBW row blocks (tblk * RBW + rbl, rbl < RBW) of kStatsThreads / 64 waves each; the
     // waves of a row block form kStreams key streams of RG waves: wave w of row block rbl
     // owns the RPW = 128 / RG rows [rg*RPW, +RPW) of it (rg = w % RG) and the key stream
@@ -206,7 +210,9 @@ __device__ __forceinline__ void stats_task(
     }
 
     const int nkb = (S + 31) >> 5;
-    const int nmine = (nkb - ks + kStreams - 1) / kStreams;     // blocks of this stream
+    const int kb_lo = __builtin_amdgcn_readfirstlane(nkb * split / nsplit);   // wave-uniform
+    const int nkb_s = __builtin_amdgcn_readfirstlane(nkb * (split + 1) / nsplit) - kb_lo;
+    const int nmine = (nkb_s - ks + kStreams - 1) / kStreams;   // blocks of this stream
     const char* kbase = reinterpret_cast<const char*>(k + ((size_t)kb0 * Hkv + g) * d);
     const int kstride = Hkv * d;                      // elements per key row
     u32x4* sring = ring + ks * RING * UNITS;
@@ -227,9 +233,11 @@ __device__ __forceinline__ void stats_task(
     }
     auto issue = [&](int j) {
         const int jj = min(j, max(nmine - 1, 0));
-        // A stream with no block of its own (nmine == 0) copies the sample's last block:
-        // every copy stays inside the sample's keys, and the stage is never read.
-        const int kbi = min(ks + jj * kStreams, nkb - 1);
+        // A stream with no block of its own (nmine == 0) copies the range's (or the
+        // sample's) last block: every copy stays inside the sample's keys, and the stage is
+        // never read.
+        const int klast = nkb_s > 0 ? kb_lo + nkb_s - 1 : nkb - 1;
+        const int kbi = min(kb_lo + ks + jj * kStreams, klast);
         const char* bbase = kbase + (size_t)kbi * 32 * kstride * 2;
         const uint32_t dst = sring_lds + (uint32_t)((jj % RING) * UNITS * 16);
         const bool full = kbi * 32 + 32 <= S;
@@ -348,7 +356,7 @@ __device__ __forceinline__ void stats_task(
 
     // Every wave runs the same number of iterations (the most any stream has), so the
     // barriers match; a stream past its last block only re-issues its last block.
-    const int iters = (nkb + kStreams - 1) / kStreams;
+    const int iters = (nkb_s + kStreams - 1) / kStreams;
     // COLSUM: the RG waves of a stream leave their column sums of block j in
     // sums[j & 1][ks][rg][key] (red_m and red_z together); after the next barrier the
     // rg = 0 wave adds them in order of rg and stores the workgroup's partial.
@@ -375,7 +383,7 @@ __device__ __forceinline__ void stats_task(
         if (COLSUM && rg == 0 && i >= 1 && i - 1 < nmine) store_sums(i - 1);
         if (i < nmine) {
             float cs = 0.f;
-            if (nsb > 0) cs = block(ks + i * kStreams, sring + (i % RING) * UNITS, i == 0);
+            if (nsb > 0) cs = block(kb_lo + ks + i * kStreams, sring + (i % RING) * UNITS, i == 0);
             if (COLSUM && hi == 0) sums[((i & 1) * kStreams + ks) * (RG * 32) + rg * 32 + lo] = cs;
         }
     }
@@ -405,7 +413,8 @@ __device__ __forceinline__ void stats_task(
         float mm = rm[i], zz = rz[i];
         for (int w = 1; w < kStreams; ++w) merge_pair(mm, zz, rm[w * kTxtRows + i], rz[w * kTxtRows + i]);
         const int t = (tblk * RBW + rr) * kTxtRows + i;
-        if (t < T) lse2[(size_t)(qb + t) * H + h] = mm + __builtin_amdgcn_logf(zz);
+        if (t < T) lse2[(size_t)split * p.lse_stride + (size_t)(qb + t) * H + h] =
+            mm + __builtin_amdgcn_logf(zz);
     }
 }
 
@@ -423,10 +432,12 @@ __global__ __launch_bounds__(kStatsThreads * RBW, 1) void text_stats_kernel(
     if (blockIdx.x == 0) clear_done(fin, p.B);
     const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
     const int ngrp = (nrb + RBW - 1) / RBW;
-    const int task = xcd_remap((int)blockIdx.x, ngrp * p.H * p.B);
-    const int tblk = task % ngrp, h = (task / ngrp) % p.H, b = task / (ngrp * p.H);
+    const int ns = COLSUM || p.lse_splits < 1 ? 1 : p.lse_splits;
+    const int task = xcd_remap((int)blockIdx.x, ngrp * p.H * p.B * ns);
+    const int split = task % ns, rest = task / ns;
+    const int tblk = rest % ngrp, h = (rest / ngrp) % p.H, b = rest / (ngrp * p.H);
     stats_task<DS, HALF, COLSUM, RG, kStatsRing, RBW>(p, q, k, lse2, lse_in, lse_natural, part,
-                                                      b, h, tblk, smem_raw);
+                                                      b, h, tblk, split, ns, smem_raw);
 }
 
 // Ragged launches: workgroup id -> the id-th non-empty (sample, key chunk, row block)
@@ -809,6 +820,26 @@ __global__ __launch_bounds__(256) void text_rows_combine_kernel(Prob p, const fl
     scores[k_begin(p, b) + s] = v;
 }
 
+// Key ranges of the statistics pass: merge the ranges' base-2 log-sum-exps, in range
+// order, into the first table (every (row, head) entry of the workspace's tables; entries
+// of rows past a sample's T_b are never read).
+__global__ __launch_bounds__(256) void text_lse_merge_kernel(Prob p, float* __restrict__ lse2,
+                                                             long long n)
+{
+    const int ns = min(p.lse_splits, kStatsMaxSplits);
+    for (long long i = (long long)blockIdx.x * 256 + threadIdx.x; i < n; i += (long long)gridDim.x * 256) {
+        float l[kStatsMaxSplits];
+        float mx = -INFINITY;
+        for (int r = 0; r < ns; ++r) {
+            l[r] = lse2[(size_t)r * p.lse_stride + i];
+            mx = fmaxf(mx, l[r]);
+        }
+        float z = 0.f;
+        for (int r = 0; r < ns; ++r) z += __builtin_amdgcn_exp2f(l[r] - mx);
+        lse2[i] = mx == -INFINITY ? mx : mx + __builtin_amdgcn_logf(z);
+    }
+}
+
 template <int DS, bool HALF, bool COLSUM, int RG, int RBW>
 static hipError_t stats_launch_rg(const Prob& p, const void* q, const void* k, float* lse2,
                                   const float* lse_in, int lse_natural, float* part,
@@ -820,10 +851,17 @@ static hipError_t stats_launch_rg(const Prob& p, const void* q, const void* k, f
         (int)kScoreSmemMax, lds_set);
     if (attr != hipSuccess) return attr;
     const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
-    dim3 grid((nrb + RBW - 1) / RBW * p.H * p.B);
-    return launch(text_stats_kernel<DS, HALF, COLSUM, RG, RBW>, grid, dim3(kStatsThreads * RBW),
-                  smem, s, p, static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
-                  lse2, lse_in, lse_natural, part, fin);
+    const int ns = COLSUM || p.lse_splits < 1 ? 1 : p.lse_splits;
+    dim3 grid((nrb + RBW - 1) / RBW * p.H * p.B * ns);
+    const hipError_t e = launch(text_stats_kernel<DS, HALF, COLSUM, RG, RBW>, grid,
+                                dim3(kStatsThreads * RBW), smem, s, p,
+                                static_cast<const uint16_t*>(q), static_cast<const uint16_t*>(k),
+                                lse2, lse_in, lse_natural, part, fin);
+    if (e != hipSuccess || ns == 1) return e;
+    const long long n = p.lse_stride;
+    const long long nblk = (n + 255) / 256;
+    return launch(text_lse_merge_kernel, dim3((unsigned)(nblk < 2048 ? nblk : 2048)), dim3(256), 0,
+                  s, p, lse2, n);
 }
 
 // Four waves of 32 rows on one key stream.  Two streams of two 64-row waves reuse each
@@ -840,11 +878,11 @@ static hipError_t stats_launch(const Prob& p, const void* q, const void* k, floa
     // one row block per workgroup: the mutual-scoring Stage I of the same batch (up to 32
     // row blocks) took 4.42 ms with four per workgroup, 3.84 ms with two, 3.83 ms with one.
     if constexpr (!COLSUM) {
-        const int nrb = (p.max_rows + kTxtRows - 1) / kTxtRows;
-        if (nrb == 3 || nrb == 4)
+        const int rbw = stats_row_blocks((p.max_rows + kTxtRows - 1) / kTxtRows);
+        if (rbw == 4)
             return stats_launch_rg<DS, HALF, COLSUM, 4, 4>(p, q, k, lse2, lse_in, lse_natural, part,
                                                            fin, s);
-        if (nrb == 2)
+        if (rbw == 2)
             return stats_launch_rg<DS, HALF, COLSUM, 4, 2>(p, q, k, lse2, lse_in, lse_natural, part,
                                                            fin, s);
     }

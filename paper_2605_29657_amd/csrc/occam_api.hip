@@ -74,8 +74,15 @@ occam_status make_plan(const occam_problem* pr, Plan* pl) {
             (R + (long long)max_cands) * x.num_kv_heads * d * 2 >= (1LL << 32))
             return OCCAM_ERR_UNSUPPORTED;
         if (text_score_smem(H, ((d + 15) / 16) * 16) > kScoreSmemMax) return OCCAM_ERR_UNSUPPORTED;
-        P.off_lse2 = off; off = align_up(off + (size_t)rows_cap * H * sizeof(float));
         const size_t nrb = (max_rows + kTxtRows - 1) / kTxtRows;
+        // The statistics pass of a small batch splits every task's keys into ranges, each
+        // with its own normaliser table (the scoring pass merges them); not for mutual scoring.
+        const int rbw = stats_row_blocks((int)nrb);
+        P.p.lse_splits = P.p.mean_rows ? 1 : stats_splits((long long)B * H * ((nrb + rbw - 1) / rbw),
+                                                           R + (long long)max_cands);
+        P.p.lse_stride = rows_cap * H;
+        P.off_lse2 = off;
+        off = align_up(off + (size_t)P.p.lse_splits * rows_cap * H * sizeof(float));
         P.off_part = off;
         if (P.p.mean_rows) {
             // Column sums of mutual scoring, per (sample, 128-row block, head, key).

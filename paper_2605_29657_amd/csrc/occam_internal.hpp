@@ -73,6 +73,8 @@ struct Prob {
     int max_rows, max_cands;  // bounds of T_b and N_b
     float scale;              // softmax temperature of Eq. (1)
     int mean_rows;            // visual keys: mean over anchor rows (1) or max (0)
+    int lse_splits;           // key ranges of the statistics pass (0 or 1: one)
+    long long lse_stride;     // floats between the ranges' normaliser tables
 };
 
 __device__ __forceinline__ int q_begin(const Prob& p, int b) {
@@ -262,6 +264,23 @@ inline size_t text_score_smem(int H, int d16) {
 // the head slices faster than deeper rings at fewer workgroups per CU: the scattered
 // 256-byte slices stream better with fewer requests outstanding per CU.
 constexpr int kStatsRing = 2;
+// Row blocks per statistics workgroup for nrb 128-row blocks per sample (at most).
+inline int stats_row_blocks(int nrb) { return nrb == 2 ? 2 : (nrb == 3 || nrb == 4) ? 4 : 1; }
+// Key ranges of the statistics pass: a batch with fewer than kStatsMinWorkgroups
+// (sample, head, row-block group) tasks splits each task's keys into up to kStatsMaxSplits
+// ranges of at least kStatsMinSplitBlocks 32-key blocks; each range writes its own base-2
+// log-sum-exp table, and the scoring pass merges them.
+constexpr int kStatsMinWorkgroups = 1024;
+constexpr int kStatsMaxSplits = 8;
+constexpr int kStatsMinSplitBlocks = 16;
+inline int stats_splits(long long tasks, long long keys) {
+    if (tasks <= 0 || tasks >= kStatsMinWorkgroups) return 1;
+    long long ks = (kStatsMinWorkgroups + tasks - 1) / tasks;
+    const long long by_keys = ((keys + 31) / 32) / kStatsMinSplitBlocks;
+    if (ks > by_keys) ks = by_keys;
+    if (ks > kStatsMaxSplits) ks = kStatsMaxSplits;
+    return ks < 1 ? 1 : (int)ks;
+}
 // rg: waves per key stream of one row block (2 or 4); rbw: row blocks per workgroup.
 inline size_t text_stats_smem(int d16, int rg, int rbw = 1) {
     return (size_t)(kStatsThreads / kWave / rg) * kStatsRing * 32 * d16 * 2 +

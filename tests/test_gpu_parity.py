@@ -271,6 +271,15 @@ def test_statistics_row_block_groups():
         run_and_check(sb, 1.2)
 
 
+def test_statistics_key_ranges():
+    # Few (sample, head) tasks with many keys: the statistics pass splits each task's keys
+    # into ranges (here 5 and 3, one of them with two row blocks per workgroup), and the
+    # scoring pass merges the ranges' normalisers.
+    for T, N, H in (([128, 70], [3000, 1500], 8), ([200, 129], [1900, 2100], 16)):
+        sb = custom_stage(B=2, R=4, H=H, Hkv=H, d=128, T=T, N=N, seed=H)
+        run_and_check(sb, 1.3)
+
+
 def test_lambda_zero_keeps_everything_and_huge_keeps_nothing():
     sb = custom_stage(B=3, R=2, H=4, Hkv=2, d=64, T=[40] * 3, N=[100] * 3)
     g, _ = run_and_check(sb, 0.0)
