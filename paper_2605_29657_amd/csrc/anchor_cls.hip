@@ -12,6 +12,10 @@
 //             partial dot products against the query held in LDS, sums them
 //             per (key, head), writes the scaled logits to the workspace and
 //             the chunk's per-head (max, sum exp) pair.
+// cls_stream / cls_stream_run  the same for H == Hkv with the query in registers:
+//             lanes own fixed 16-byte slots of the key rows (heads padded to a power
+//             of two of lanes), or, for 16 heads of 5-7 or 9 chunks, contiguous runs
+//             of four key rows with the per-(row, head) sums formed through LDS.
 // cls_scores  grid (key chunk, sample): merges the per-chunk pairs of the
 //             sample into the softmax normaliser of every head (fixed order),
 //             then score(s) = (1/H) sum_h exp(l[s,h] - m_h) / z_h.
@@ -278,6 +282,131 @@ __global__ __launch_bounds__(kClsThreads) void cls_stream_kernel(
     }
 }
 
+// Streaming form for 16 heads whose chunk count NCK is not a power of two (d = 72 in
+// bfloat16: nine 16-byte chunks per head).  Padding a head to 16 lanes, as
+// cls_stream_kernel does, would have 7 of every 16 lanes reread a chunk; instead a wave
+// reads KB = 4 consecutive key rows as one contiguous run of 4 * 16 * NCK chunks, NCK
+// coalesced 1 KB loads per lane with no lane idle, and forms each chunk's partial dot
+// product.  The partials go to the wave's own LDS row, and lane L = (row r = L / 16,
+// head h = L % 16) adds the NCK partials of its (row, head) in chunk order, writes the
+// scaled logit and folds it into its online (max, sum exp) pair; the 16 pairs of a head
+// (4 waves x 4 rows) are merged in a fixed order at the end.
+template <bool BF16, int NCK>
+__global__ __launch_bounds__(kClsThreads) void cls_stream_run_kernel(
+    Prob p, const void* __restrict__ qv, const void* __restrict__ kv,
+    float* __restrict__ logits, float2* __restrict__ stats, int kpw, int nchunks, Finish fin)
+{
+    constexpr int CE = BF16 ? 8 : 4;                 // elements per 16-byte chunk
+    constexpr int HH = 16;                           // heads: 4 rows x 16 heads = 64 lanes
+    constexpr int KB = 4;                            // key rows per wave step
+    constexpr int ROWC = HH * NCK;                   // 16-byte chunks per key row
+    constexpr int NJ = KB * ROWC / kWave;            // loads per lane per step (= NCK)
+    static_assert((KB * ROWC) % kWave == 0, "a run of KB rows fills whole wave loads");
+    constexpr int NW = kClsThreads / kWave;
+    __shared__ float part[NW][KB * ROWC];
+    __shared__ float red_m[NW][kWave], red_z[NW][kWave];
+    const int c = blockIdx.x, b = blockIdx.y;
+    if (c == 0 && b == 0) clear_done(fin, p.B);      // counters of the cls_scores launch
+    const int S = keys_of(p, b);
+    const int s0 = c * kpw;
+    if (s0 >= S) return;                             // uniform over the workgroup
+    const int nk = min(kpw, S - s0);
+    const int d = p.d;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const float scale = p.scale;
+
+    // Query elements of the chunk each load of this lane reads (the same for every run:
+    // chunk cc = 64 j + lane of the run is column cc % ROWC of its row).
+    float qf[NJ][CE];
+    const int qrow = q_begin(p, b);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int col = (j * kWave + lane) % ROWC;
+        const int h = col / NCK, e0 = (col % NCK) * CE;
+        if constexpr (BF16) {
+            const uint16_t* q16 = static_cast<const uint16_t*>(qv) + ((size_t)qrow * HH + h) * d + e0;
+#pragma unroll
+            for (int e = 0; e < CE; ++e) qf[j][e] = __uint_as_float(static_cast<uint32_t>(q16[e]) << 16);
+        } else {
+            const float* q32 = static_cast<const float*>(qv) + ((size_t)qrow * HH + h) * d + e0;
+#pragma unroll
+            for (int e = 0; e < CE; ++e) qf[j][e] = q32[e];
+        }
+    }
+
+    const int rr = lane / HH, hh = lane % HH;        // this lane's (row of the run, head)
+    float m = -INFINITY, z = 0.f;
+    const u32x4* kbase = static_cast<const u32x4*>(kv) + ((size_t)k_begin(p, b) + s0) * ROWC;
+    float* lout = logits + ((size_t)k_begin(p, b) + s0) * HH;
+    float* prt = part[wave];
+
+    for (int k0 = wave * KB; k0 < nk; k0 += NW * KB) {
+        u32x4 w[NJ];
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            const int cc = j * kWave + lane;
+            const int key = min(k0 + cc / ROWC, nk - 1);    // clamped rows are loaded, not used
+            w[j] = __builtin_nontemporal_load(kbase + (size_t)key * ROWC + cc % ROWC);
+        }
+#pragma unroll
+        for (int j = 0; j < NJ; ++j) {
+            float kf[CE];
+            if constexpr (BF16) {
+                kf[0] = bf16_lo(w[j].x); kf[1] = bf16_hi(w[j].x);
+                kf[2] = bf16_lo(w[j].y); kf[3] = bf16_hi(w[j].y);
+                kf[4] = bf16_lo(w[j].z); kf[5] = bf16_hi(w[j].z);
+                kf[6] = bf16_lo(w[j].w); kf[7] = bf16_hi(w[j].w);
+            } else {
+                kf[0] = __uint_as_float(w[j].x); kf[1] = __uint_as_float(w[j].y);
+                kf[2] = __uint_as_float(w[j].z); kf[3] = __uint_as_float(w[j].w);
+            }
+            float acc = 0.f;
+#pragma unroll
+            for (int e = 0; e < CE; ++e) acc = fmaf(qf[j][e], kf[e], acc);
+            prt[j * kWave + lane] = acc;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        float l = 0.f;
+#pragma unroll
+        for (int sc = 0; sc < NCK; ++sc) l += prt[rr * ROWC + hh * NCK + sc];
+        l *= scale;
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();             // reads done before the next step's writes
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (k0 + rr < nk) {
+            lout[(size_t)(k0 + rr) * HH + hh] = l;
+            if (l > m) {
+                z = z * cls_exp<BF16>(m - l) + 1.f;
+                m = l;
+            } else {
+                z += cls_exp<BF16>(l - m);
+            }
+        }
+    }
+
+    // Fixed-order merge of the 16 pairs of each head (waves, then rows; (-inf, 0) for a
+    // row slot that saw no key).
+    red_m[wave][lane] = m;
+    red_z[wave][lane] = z;
+    __syncthreads();
+    if (threadIdx.x < HH) {
+        const int h = threadIdx.x;
+        float mm = -INFINITY, zz = 0.f;
+        for (int w2 = 0; w2 < NW; ++w2)
+            for (int r = 0; r < KB; ++r) {
+                const float mo = red_m[w2][r * HH + h], zo = red_z[w2][r * HH + h];
+                const float mn = fmaxf(mm, mo);
+                if (mn != -INFINITY) {
+                    zz = zz * cls_exp<BF16>(mm - mn) + zo * cls_exp<BF16>(mo - mn);
+                    mm = mn;
+                }
+            }
+        stats[((size_t)b * nchunks + c) * HH + h] = make_float2(mm, zz);
+    }
+}
+
 // score(s) of one key from its H logits and the per-head normalisers: the one
 // expression both the scores and the per-chunk threshold use, so that they agree bit for
 // bit.
@@ -429,6 +558,17 @@ hipError_t launch_cls_logits(const Prob& p, int bf16, const void* q, const void*
                              float* logits, float2* stats, int kpw, const Finish& fin,
                              hipStream_t s)
 {
+    if (bf16 && p.H == 16 && p.Hkv == 16 && (p.d == 72 || p.d == 40 || p.d == 48 || p.d == 56)) {
+        // 16 heads of 9 (5, 6, 7) chunks: contiguous runs of four key rows.
+        const int nchunks = (p.R + p.max_cands + kpw - 1) / kpw;
+        const dim3 grid(nchunks, p.B), blk(kClsThreads);
+        switch (p.d) {
+        case 40: return launch(cls_stream_run_kernel<true, 5>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, fin);
+        case 48: return launch(cls_stream_run_kernel<true, 6>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, fin);
+        case 56: return launch(cls_stream_run_kernel<true, 7>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, fin);
+        default: return launch(cls_stream_run_kernel<true, 9>, grid, blk, 0, s, p, q, k, logits, stats, kpw, nchunks, fin);
+        }
+    }
     const int nc = cls_stream_nc(p.H, p.Hkv, p.d, bf16 ? 2 : 4);
     if (nc) {
         return bf16 ? cls_stream_nc_launch<true>(p, nc, q, k, logits, stats, kpw, fin, s)

@@ -280,6 +280,15 @@ def test_statistics_key_ranges():
         run_and_check(sb, 1.3)
 
 
+def test_cls_row_odd_head_chunks():
+    # One anchor row, 16 heads of 5, 6, 7 or 9 sixteen-byte chunks (d = 40, 48, 56, 72):
+    # the key rows stream as contiguous runs of four rows; ragged, with an empty sample and
+    # a chunk that ends after one key.
+    for d in (40, 48, 56, 72):
+        sb = custom_stage(B=4, R=4, H=16, Hkv=16, d=d, T=[1] * 4, N=[300, 0, 1021, 125], seed=d)
+        run_and_check(sb, 0.9)
+
+
 def test_lambda_zero_keeps_everything_and_huge_keeps_nothing():
     sb = custom_stage(B=3, R=2, H=4, Hkv=2, d=64, T=[40] * 3, N=[100] * 3)
     g, _ = run_and_check(sb, 0.0)
