@@ -37,9 +37,7 @@
 //             global -> LDS (double-buffered) and the wave's key fragments are
 //             loaded into registers one head ahead, while p = 2^(x - lse2) of the
 //             current head is accumulated over heads per (key, row); the workgroups
-//             of one XCD walk the heads from the same start, and take a sample's
-//             key chunks last one first (the keys the statistics pass read last
-//             are still in the memory-side cache).  Afterwards the row
+//             of one XCD walk the heads from the same start.  Afterwards the row
 //             reduction of Eq. text_scoring is applied: max over rows for visual
 //             keys, mean for registers, both over the head mean (1/H); with several
 //             row blocks the per-block maxima and sums are combined by the sample's
@@ -760,21 +758,8 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     } else {
         const int task = xcd_remap((int)blockIdx.x, nchunk * nrb * p.B);
         rb = task % nrb;
-        if (p.lse_splits <= 1) {
-            // Each XCD's range holds G consecutive samples (in reverse order).  Inside it the
-            // chunks go from the last to the first, the samples of the group side by side:
-            // the statistics pass walks every sample's keys from the first block to the last,
-            // so the last chunks are the keys the 256 MB memory-side cache still holds, and
-            // the first workgroups on the chip read them before new misses push them out.
-            const int G = (p.B + kXcds - 1) / kXcds, per = G * nchunk * nrb;
-            const int g = task / per, cs = (task - g * per) / nrb;
-            const int gs = min(G, p.B - g * G);
-            c = nchunk - 1 - cs / gs;
-            b = p.B - 1 - (g * G + cs % gs);
-        } else {
-            c = (task / nrb) % nchunk;
-            b = p.B - 1 - task / (nrb * nchunk);
-        }
+        c = (task / nrb) % nchunk;
+        b = p.B - 1 - task / (nrb * nchunk);
     }
     // The starting head follows the XCD (workgroups are dealt to the 8 XCDs round-robin,
     // and each XCD runs one contiguous range of tasks): every workgroup of an XCD walks the
