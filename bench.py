@@ -52,6 +52,23 @@ def settle(torch, fn, seconds: float = 0.05, min_calls: int = 10):
     return n
 
 
+# Input copies that consecutive timed calls cycle through.  Each copy has its own input,
+# output and workspace buffers, so a call never reads keys that the call before it left in
+# the 256 MB memory-side cache, as with a batch of new images every step; three copies keep
+# the working set between two uses of one copy above the cache's size at every shape here.
+NCOPY = 3
+
+
+def cycler(fns):
+    """One callable that runs fns[0], fns[1], ..., fns[-1], fns[0], ... in turn."""
+    it = [0]
+
+    def one():
+        fns[it[0] % len(fns)]()
+        it[0] += 1
+    return one
+
+
 def stage_bytes(sb, kept_per_sample) -> dict:
     """Algorithmic HBM bytes of one fused prune over a batch.
 
@@ -140,7 +157,8 @@ def mutual_stage1(torch, steps: int, warmup: int, with_cpu: bool) -> dict:
     """The mutual-scoring Stage I (Eq. mutual_scoring) on the Qwen3-VL-shaped batch: every
     register and visual token is an anchor row.  Fused prune with the hidden-row gather,
     timed alone; its work is (R+N)^2 * H * d per sample, so it is graded against the bf16
-    MFMA peak (algorithmic flops count one Q K^T)."""
+    MFMA peak (algorithmic flops count one Q K^T).  The calls cycle through NCOPY input
+    copies."""
     import oracle
     from paper_2605_29657_amd import synth
     from paper_2605_29657_amd.runner import DeviceStage
@@ -148,14 +166,16 @@ def mutual_stage1(torch, steps: int, warmup: int, with_cpu: bool) -> dict:
     with open(os.path.join(ROOT, "tests", "golden", "lambdas.json")) as f:
         lam = float(np.float32(json.load(f)[name]["mut"]["lam"]))
     sb = synth.make_stage(name, "mut")
-    ds = DeviceStage(sb, ragged=True)
+    dss = [DeviceStage(sb, ragged=True) for _ in range(NCOPY)]
+    ds = dss[0]
+    call = cycler([(lambda d=d: d.prune(lam)) for d in dss])
     for _ in range(warmup):
-        ds.prune(lam)
-    settle(torch, lambda: ds.prune(lam))
+        call()
+    settle(torch, call)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
     for _ in range(steps):
-        ds.prune(lam)
+        call()
     e1.record()
     torch.cuda.synchronize()
     ms = e0.elapsed_time(e1) / steps
@@ -284,7 +304,7 @@ def budget_matching_bench(torch, reps: int = 20) -> dict:
             "ratios_per_us": round(B * N / (ms * 1e3), 1)}
 
 
-def ablation_steps(torch, dv, dt, k1: float, k2: float, steps: int) -> dict:
+def ablation_steps(torch, dvs, dts, k1: float, k2: float, steps: int) -> dict:
     """The component ablation's two threshold variants (Table
     tab:qwen_compact_component_ablation) on the headline batch, each at the register
     rule's mean budgets k1 / k2 (the paper compares variants at matched retention):
@@ -293,8 +313,11 @@ def ablation_steps(torch, dv, dt, k1: float, k2: float, steps: int) -> dict:
       visual score as reference) to k1 / k2, then the same fused prune of both stages;
     * fixed budget: occam_score, occam_select_topk with K = round(k1) / round(k2), and
       occam_gather of the same rows.
+
+    Both steps cycle through the input copies dvs / dts (Stage I / Stage II).
     """
     from paper_2605_29657_amd import occam
+    dv, dt = dvs[0], dts[0]
     lam = torch.empty(2, dtype=torch.float32, device="cuda")
     mk = torch.empty(2, dtype=torch.float32, device="cuda")
     for i, (ds, k) in enumerate(((dv, k1), (dt, k2))):
@@ -304,9 +327,9 @@ def ablation_steps(torch, dv, dt, k1: float, k2: float, steps: int) -> dict:
     lam1, lam2 = lam.cpu().tolist()
     K1, K2 = int(round(k1)), int(round(k2))
 
-    def mean_step():
-        dv.prune(lam1, reduce=occam.REF_CAND_MEAN)
-        dt.prune(lam2, reduce=occam.REF_CAND_MEAN)
+    mean_step = cycler([(lambda a=a, b=b: (a.prune(lam1, reduce=occam.REF_CAND_MEAN),
+                                           b.prune(lam2, reduce=occam.REF_CAND_MEAN)))
+                        for a, b in zip(dvs, dts)])
 
     def topk(ds, K):
         o = ds.out
@@ -315,9 +338,7 @@ def ablation_steps(torch, dv, dt, k1: float, k2: float, steps: int) -> dict:
                           o["kept_offsets"], ds.ws)
         occam.gather(ds.problem, ds.rows, o["kept_idx"], o["kept_offsets"])
 
-    def topk_step():
-        topk(dv, K1)
-        topk(dt, K2)
+    topk_step = cycler([(lambda a=a, b=b: (topk(a, K1), topk(b, K2))) for a, b in zip(dvs, dts)])
 
     def timed(fn, n):
         settle(torch, fn)
@@ -378,11 +399,13 @@ def chained_stage(txt, kept_idx, kept_offsets):
                             q=txt.q, k=txt.k[krows], payload=payload)
 
 
-def stage_breakdown(torch, dv, dt, txt, lam1: float, lam2: float, steps: int) -> dict:
+def stage_breakdown(torch, dvs, dts, txt, lam1: float, lam2: float, steps: int) -> dict:
     """Each stage alone, and the chained pipeline: Stage II over the R + N1 tokens that
     Stage I kept (its keys and payload rows staged untimed), index_map = Stage I's
-    indices, so that Stage II reports original token indices."""
+    indices, so that Stage II reports original token indices.  Every timing cycles
+    through input copies (dvs / dts for the two stages)."""
     from paper_2605_29657_amd.runner import DeviceStage
+    from paper_2605_29657_amd import occam
 
     def timed(fn, n):
         settle(torch, fn)
@@ -394,53 +417,38 @@ def stage_breakdown(torch, dv, dt, txt, lam1: float, lam2: float, steps: int) ->
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / n
 
-    from paper_2605_29657_amd import occam
+    def input_bytes(ds):
+        return (int(ds.q.numel() + ds.k.numel()) * ds.k.element_size() +
+                sum(int(r.numel()) * r.element_size() for r in ds.row_src))
 
-    def timed_rot(fns, n):
-        # Consecutive calls cycle through copies of the input on distinct buffers, so that
-        # a working set smaller than the 256 MB memory-side cache is not served from it.
-        it = [0]
-
-        def one():
-            fns[it[0] % len(fns)]()
-            it[0] += 1
-        settle(torch, one)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for i in range(n):
-            fns[i % len(fns)]()
-        e1.record()
-        torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / n
-
+    dv, dt = dvs[0], dts[0]
     B = dv.sb.B
-    # Stage I touches ~260 MB per call (keys 189 MB, gather 68 MB): three copies (~770 MB
-    # of inputs) rotate.  Stage II reads 790 MB of keys and queries per call, more than the
-    # cache holds, so it runs on one copy.
-    copies = [dv] + [DeviceStage(dv.sb, ragged=dv.ragged) for _ in range(2)]
-    ms1 = timed_rot([(lambda d=d: d.prune(lam1)) for d in copies], steps)
-    ms2 = timed(lambda: dt.prune(lam2), steps)
+    ms1 = timed(cycler([(lambda d=d: d.prune(lam1)) for d in dvs]), steps)
+    ms2 = timed(cycler([(lambda d=d: d.prune(lam2)) for d in dts]), steps)
     b1 = stage_bytes(dv.sb, dv.out["kept_count"].cpu().numpy())["total"]
     b2 = stage_bytes(dt.sb, dt.out["kept_count"].cpu().numpy())["total"]
     # Stage I scoring alone (occam_score: the one-row logits with online statistics, then
     # the scores): reads every key once, writes one score per key.
-    scs = [torch.empty_like(dv.out["scores"]) for _ in copies]
-    ms1s = timed_rot([(lambda d=d, o=o: occam.score(d.problem, d.q, d.k, o, d.ws))
-                      for d, o in zip(copies, scs)], steps)
-    rot_bytes = sum(int(d.q.numel() + d.k.numel()) * d.k.element_size() +
-                    sum(int(r.numel()) * r.element_size() for r in d.row_src) for d in copies)
-    del copies[1:], scs
+    scs = [torch.empty_like(dv.out["scores"]) for _ in dvs]
+    ms1s = timed(cycler([(lambda d=d, o=o: occam.score(d.problem, d.q, d.k, o, d.ws))
+                         for d, o in zip(dvs, scs)]), steps)
+    del scs
     e1 = 2 if dv.sb.dtype == "bf16" else 4
     bs1 = int(dv.sb.k_off[-1]) * (dv.sb.Hkv * dv.sb.d * e1 + 4) + int(dv.sb.q_off[-1]) * dv.sb.H * dv.sb.d * e1
     kept_idx = dv.out["kept_idx"].cpu().numpy()
     kept_off = dv.out["kept_offsets"].cpu().numpy()
     ch = chained_stage(txt, kept_idx, kept_off)
     # Every sample keeps its T text rows; only the key counts are ragged.
-    dc = DeviceStage(ch, ragged=True, row_offsets=not bool(np.all(ch.T == ch.T[0])))
+    dcs = [DeviceStage(ch, ragged=True, row_offsets=not bool(np.all(ch.T == ch.T[0])))
+           for _ in range(len(dts))]
     imap = dv.out["kept_idx"][:int(kept_off[-1])].clone()
-    ms2c = timed(lambda: dc.prune(lam2, index_map=imap), steps)
-    kept2c = dc.out["kept_count"].float().mean().item()
-    del dc
+    ms2c = timed(cycler([(lambda d=d: d.prune(lam2, index_map=imap)) for d in dcs]), steps)
+    kept2c = dcs[0].out["kept_count"].float().mean().item()
+    rot = "each timing cycles through %d input copies (Stage I %d MB, Stage II %d MB, " \
+          "chained Stage II %d MB of inputs in all)" % (
+              len(dvs), sum(map(input_bytes, dvs)) // 10**6, sum(map(input_bytes, dts)) // 10**6,
+              sum(map(input_bytes, dcs)) // 10**6)
+    del dcs
     gbs = lambda nbytes, ms: nbytes / (ms * 1e-3) / 1e9
     return {"stage1_ms": round(ms1, 4), "stage2_ms": round(ms2, 4),
             "stage1_hbm_gbs": round(gbs(b1, ms1), 1),
@@ -450,7 +458,7 @@ def stage_breakdown(torch, dv, dt, txt, lam1: float, lam2: float, steps: int) ->
             "stage1_score": {"ms": round(ms1s, 4), "bytes": bs1,
                              "hbm_gbs": round(gbs(bs1, ms1s), 1),
                              "hbm_frac": round(gbs(bs1, ms1s) / HBM_PEAK_GBS, 4)},
-            "stage1_rotation": "3 input copies, %d MB of inputs" % (rot_bytes // 10**6),
+            "rotation": rot,
             "chained": {"stage2_keys_mean": float(np.mean(ch.N + ch.R)),
                         "stage2_ms": round(ms2c, 4), "step_ms": round(ms1 + ms2c, 4),
                         "images_s": round(B / ((ms1 + ms2c) * 1e-3), 1),
@@ -462,7 +470,8 @@ def workload_step(torch, name: str, steps: int) -> dict:
     workload shape: images/s, the step's algorithmic bytes over its time, and the text
     stage's algorithmic MFMA rate (one Q K^T) over the step; then the text stage alone
     (its Q K^T rate, and with both passes' Q K^T), also for the samples with at least 312
-    text rows when the batch mixes row counts."""
+    text rows when the batch mixes row counts.  Every timing cycles through NCOPY input
+    copies."""
     from paper_2605_29657_amd import synth
     from paper_2605_29657_amd.runner import DeviceStage
     with open(os.path.join(ROOT, "tests", "golden", "lambdas.json")) as f:
@@ -471,13 +480,10 @@ def workload_step(torch, name: str, steps: int) -> dict:
     lam2 = float(np.float32(lams["txt"]["lam"]))
     vis = synth.make_stage(name, "vis")
     txt = synth.make_stage(name, "txt")
-    dv = DeviceStage(vis, ragged=vis.ragged)
-    dt = DeviceStage(txt, ragged=txt.ragged)
-
-    def step():
-        dv.prune(lam1)
-        dt.prune(lam2)
-
+    dvs = [DeviceStage(vis, ragged=vis.ragged) for _ in range(NCOPY)]
+    dts = [DeviceStage(txt, ragged=txt.ragged) for _ in range(NCOPY)]
+    dv, dt = dvs[0], dts[0]
+    step = cycler([(lambda a=a, b=b: (a.prune(lam1), b.prune(lam2))) for a, b in zip(dvs, dts)])
     settle(torch, step)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     e0.record()
@@ -500,8 +506,8 @@ def workload_step(torch, name: str, steps: int) -> dict:
            "text_mfma_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
            "kept_stage1_mean": float(np.mean(kept1)), "kept_stage2_mean": float(np.mean(kept2))}
 
-    def text_stage(sb, ds):
-        fn = lambda: ds.prune(lam2)
+    def text_stage(sb, dss):
+        fn = cycler([(lambda d=d: d.prune(lam2)) for d in dss])
         settle(torch, fn)
         e0.record()
         for _ in range(steps):
@@ -515,14 +521,14 @@ def workload_step(torch, name: str, steps: int) -> dict:
                 "mfma_frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4),
                 "two_pass_mfma_frac": round(2 * tf / MFMA_BF16_PEAK_TFLOPS, 4)}
 
-    out["text_stage"] = text_stage(txt, dt)
-    del dv, dt
+    out["text_stage"] = text_stage(txt, dts)
+    del dv, dt, dvs, dts
     big = [b for b in range(txt.B) if txt.T[b] >= 312]
     if big and len(big) < txt.B:
         sub = synth.make_stage(name, "txt", samples=big)
-        ds = DeviceStage(sub, ragged=sub.ragged)
-        out["text_stage"]["t_ge_312"] = text_stage(sub, ds)
-        del ds
+        dss = [DeviceStage(sub, ragged=sub.ragged) for _ in range(NCOPY)]
+        out["text_stage"]["t_ge_312"] = text_stage(sub, dss)
+        del dss
     torch.cuda.empty_cache()
     return out
 
@@ -799,14 +805,14 @@ def main():
     vis = synth.make_stage(name, "vis")
     txt = synth.make_stage(name, "txt")
     log("generated %s in %.1fs" % (name, time.time() - t0))
-    dv = DeviceStage(vis, ragged=vis.ragged)
-    dt = DeviceStage(txt, ragged=txt.ragged)
+    # Consecutive steps cycle through NCOPY copies of both stages' inputs (the step of a
+    # serving loop sees a new batch of images every time).
+    dvs = [DeviceStage(vis, ragged=vis.ragged) for _ in range(NCOPY)]
+    dts = [DeviceStage(txt, ragged=txt.ragged) for _ in range(NCOPY)]
+    dv, dt = dvs[0], dts[0]
     torch.cuda.synchronize()
     B = vis.B
-
-    def step():
-        dv.prune(lam1)
-        dt.prune(lam2)
+    step = cycler([(lambda a=a, b=b: (a.prune(lam1), b.prune(lam2))) for a, b in zip(dvs, dts)])
 
     # Device warm-up before the W warm-up steps: freshly staged buffers are touched for the
     # first time and the clocks leave their idle state; measured from a cold start, the
@@ -836,6 +842,20 @@ def main():
     ms = e0.elapsed_time(e1) / args.steps
     log("timed %d steps: %.3f ms/step (wall %.3f ms/step)" % (args.steps, ms,
                                                               wall * 1e3 / args.steps))
+    # For reference: the same steps all on one copy, so that each step's statistics pass
+    # can find keys that the previous step left in the memory-side cache.
+    def step_one_copy():
+        dv.prune(lam1)
+        dt.prune(lam2)
+
+    settle(torch, step_one_copy)
+    e0.record()
+    for _ in range(args.steps):
+        step_one_copy()
+    e1.record()
+    torch.cuda.synchronize()
+    ms_one = e0.elapsed_time(e1) / args.steps
+    log("the same steps on one input copy: %.3f ms/step" % ms_one)
 
     b1 = stage_bytes(vis, kept1)
     b2 = stage_bytes(txt, kept2)
@@ -847,21 +867,27 @@ def main():
     # normaliser launches exactly that one kernel, so HIP events around the call on the
     # launch stream time it alone.  The normaliser is the true per-(row, head) log-sum-exp
     # (float32 matmul on the device; setup only).
+    # The calls cycle through the input copies; the normaliser (identical for all copies)
+    # is one tensor.
     lse = reference_lse(torch, txt, dt)
-    scores_buf = torch.empty_like(dt.out["scores"])
-    settle(torch, lambda: occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws, row_lse=lse))
+    score_bufs = [torch.empty_like(d.out["scores"]) for d in dts]
+    score_alone = cycler([(lambda d=d, o=o: occam.score(d.problem, d.q, d.k, o, d.ws, row_lse=lse))
+                          for d, o in zip(dts, score_bufs)])
+    settle(torch, score_alone)
     k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     k0.record()
     for _ in range(args.kernel_reps):
-        occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws, row_lse=lse)
+        score_alone()
     k1.record()
     torch.cuda.synchronize()
     score_ms = k0.elapsed_time(k1) / args.kernel_reps
     # Both Stage II passes (statistics + scoring) for reference.
-    settle(torch, lambda: occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws))
+    both = cycler([(lambda d=d, o=o: occam.score(d.problem, d.q, d.k, o, d.ws))
+                   for d, o in zip(dts, score_bufs)])
+    settle(torch, both)
     k0.record()
     for _ in range(args.kernel_reps):
-        occam.score(dt.problem, dt.q, dt.k, scores_buf, dt.ws)
+        both()
     k1.record()
     torch.cuda.synchronize()
     both_ms = k0.elapsed_time(k1) / args.kernel_reps
@@ -873,10 +899,8 @@ def main():
 
     # The same step when the caller supplies the Stage II row normalisers (the LLM's own
     # attention log-sum-exp, mode row_lse): Stage II is then the scoring pass alone.
-    def step_lse():
-        dv.prune(lam1)
-        dt.prune(lam2, row_lse=lse)
-
+    step_lse = cycler([(lambda a=a, b=b: (a.prune(lam1), b.prune(lam2, row_lse=lse)))
+                       for a, b in zip(dvs, dts)])
     settle(torch, step_lse)
     k0.record()
     for _ in range(args.steps):
@@ -895,20 +919,21 @@ def main():
     # into occam_score (exactly text_score here), occam_threshold, occam_select and
     # occam_gather, HIP events on the launch stream around the scoring call of every step,
     # so that Stage I's traffic precedes it as in the step.
-    o = dt.out
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(args.steps)]
     for i in range(-3, args.steps):
-        dv.prune(lam1)
+        a, d = dvs[i % NCOPY], dts[i % NCOPY]
+        o = d.out
+        a.prune(lam1)
         if i >= 0:
             ev[i][0].record()
-        occam.score(dt.problem, dt.q, dt.k, o["scores"], dt.ws, row_lse=lse)
+        occam.score(d.problem, d.q, d.k, o["scores"], d.ws, row_lse=lse)
         if i >= 0:
             ev[i][1].record()
-        occam.threshold(dt.problem, o["scores"], lam2, occam.REG_MEAN, o["tau"])
-        occam.select(dt.problem, o["scores"], o["tau"], o["kept_idx"], o["kept_count"],
-                     o["kept_offsets"], dt.ws)
-        occam.gather(dt.problem, dt.rows, o["kept_idx"], o["kept_offsets"])
+        occam.threshold(d.problem, o["scores"], lam2, occam.REG_MEAN, o["tau"])
+        occam.select(d.problem, o["scores"], o["tau"], o["kept_idx"], o["kept_count"],
+                     o["kept_offsets"], d.ws)
+        occam.gather(d.problem, d.rows, o["kept_idx"], o["kept_offsets"])
     torch.cuda.synchronize()
     in_step_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     log("text_score inside the caller-normaliser step: %.3f ms" % in_step_ms)
@@ -945,6 +970,9 @@ def main():
         "hbm_frac": round(step_gbs / HBM_PEAK_GBS, 4),
         "step_bytes": step_bytes,
         "device_warmup_steps": settle_steps,
+        "inputs": "each timed step (and every other timing below, unless stated) cycles through "
+                  "%d copies of both stages' inputs, outputs and workspaces" % NCOPY,
+        "one_copy_ms_per_step": round(ms_one, 4),
         "roofline": {"kernel": "text_score", "bound": "hbm", "achieved": round(achieved, 1),
                      "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic, "avg_ms": round(score_ms, 4),
@@ -967,20 +995,21 @@ def main():
     log("register redirect: %.1f us" % rec["register_redirect"]["us"])
     rec["budget_matching"] = budget_matching_bench(torch)
     log("budget matching: %.1f us" % rec["budget_matching"]["us"])
-    rec["stages"] = stage_breakdown(torch, dv, dt, txt, lam1, lam2, max(10, args.steps // 2))
+    rec["stages"] = stage_breakdown(torch, dvs, dts, txt, lam1, lam2, max(10, args.steps // 2))
     log("stage I alone %.3f ms (%.1f%% of HBM peak; its scoring %.1f%%), stage II alone %.3f ms "
         "(%.1f%%); chained step %.3f ms (%.0f keys)" % (
             rec["stages"]["stage1_ms"], 100 * rec["stages"]["stage1_hbm_frac"],
             100 * rec["stages"]["stage1_score"]["hbm_frac"], rec["stages"]["stage2_ms"],
             100 * rec["stages"]["stage2_hbm_frac"], rec["stages"]["chained"]["step_ms"],
             rec["stages"]["chained"]["stage2_keys_mean"]))
-    rec["ablation"] = ablation_steps(torch, dv, dt, float(kept1.mean()), float(kept2.mean()),
+    rec["ablation"] = ablation_steps(torch, dvs, dts, float(kept1.mean()), float(kept2.mean()),
                                      max(10, args.steps // 2))
     log("ablation: mean threshold %.3f ms/step, fixed budget %.3f ms/step" % (
         rec["ablation"]["mean_threshold"]["ms_per_step"],
         rec["ablation"]["fixed_budget"]["ms_per_step"]))
+    del score_bufs, score_alone, both, step, step_lse, a, d, o
     if not args.no_workloads:
-        del dv, dt
+        del dv, dt, dvs, dts
         torch.cuda.empty_cache()
         rec["workloads"] = {}
         for wname in ("llava15", "qwen3vl_ragged", "video"):
@@ -989,7 +1018,7 @@ def main():
                 wname, rec["workloads"][wname]["ms_per_step"], rec["workloads"][wname]["images_s"],
                 100 * rec["workloads"][wname]["hbm_frac"]))
     if not args.no_mutual:
-        dv = dt = None
+        dv = dt = dvs = dts = None
         torch.cuda.empty_cache()
         rec["mutual_stage1"] = mutual_stage1(torch, max(5, args.steps // 5), 2,
                                              not args.no_cpu_baseline)
