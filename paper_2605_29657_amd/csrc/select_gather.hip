@@ -174,9 +174,10 @@ __global__ __launch_bounds__(kGatherThreads) void pack_gather_kernel(
         const long long nb = rt.row_bytes;
         if (rows.vec16) {
             // Four 16-byte loads in flight per lane before the stores.  The copies are
-            // non-temporal: the rows are touched once, and allocating them in the 256 MB
-            // memory-side cache would evict the keys that the next statistics pass reads
-            // again (measured: the LLaVA-NeXT step 16 us shorter, 0.437 -> 0.421 ms).
+            // non-temporal: the rows are touched once, and without the hint they would
+            // take room in the 256 MB memory-side cache and leave dirty lines there
+            // (measured with the steps cycling through three input copies: the
+            // LLaVA-NeXT step 0.437 -> 0.428 ms).
             // A 2 KB row (Stage I hidden states) is two loads per lane, both issued
             // before either store.
             constexpr long long step = 16 * kWave;
