@@ -444,6 +444,30 @@ def stage_breakdown(torch, dvs, dts, txt, lam1: float, lam2: float, steps: int) 
     imap = dv.out["kept_idx"][:int(kept_off[-1])].clone()
     ms2c = timed(cycler([(lambda d=d: d.prune(lam2, index_map=imap)) for d in dcs]), steps)
     kept2c = dcs[0].out["kept_count"].float().mean().item()
+    # The gathers alone (occam_gather over each copy's kept lists: the same pack_gather
+    # kernel), next to a plain contiguous device copy of the same bytes, the copy's source
+    # and destination cycling through enough buffers (>= 1.2 GB) that the memory-side
+    # cache holds none of them.
+    def gather_vs_copy(dss):
+        sb = dss[0].sb
+        kept = dss[0].out["kept_count"].cpu().numpy()
+        nbytes = (stage_bytes(sb, kept)["gather"] - 4 * int(kept.sum())) // 2
+        us = timed(cycler([(lambda d=d: occam.gather(d.problem, d.rows, d.out["kept_idx"],
+                                                      d.out["kept_offsets"])) for d in dss]),
+                   steps) * 1e3
+        nb = max(3, -(-1200 * 10**6 // max(nbytes, 1)))
+        bufs = [(torch.empty(nbytes, dtype=torch.uint8, device="cuda"),
+                 torch.empty(nbytes, dtype=torch.uint8, device="cuda")) for _ in range(nb)]
+        cus = timed(cycler([(lambda a=a, b=b: b.copy_(a)) for a, b in bufs]), steps) * 1e3
+        del bufs
+        return {"row_bytes_read": nbytes, "gather_us": round(us, 2), "copy_us": round(cus, 2),
+                "gather_tbs": round(2 * nbytes / (us * 1e-6) / 1e12, 2),
+                "copy_tbs": round(2 * nbytes / (cus * 1e-6) / 1e12, 2),
+                "gather_vs_copy": round(cus / us, 3)}
+
+    gathers = {"stage1": gather_vs_copy(dvs), "stage2": gather_vs_copy(dts),
+               "how": "occam_gather alone (the pack_gather kernel) against a contiguous device "
+                      "copy of the same bytes; TB/s count reads + writes"}
     rot = "each timing cycles through %d input copies (Stage I %d MB, Stage II %d MB, " \
           "chained Stage II %d MB of inputs in all)" % (
               len(dvs), sum(map(input_bytes, dvs)) // 10**6, sum(map(input_bytes, dts)) // 10**6,
@@ -459,6 +483,7 @@ def stage_breakdown(torch, dvs, dts, txt, lam1: float, lam2: float, steps: int) 
                              "hbm_gbs": round(gbs(bs1, ms1s), 1),
                              "hbm_frac": round(gbs(bs1, ms1s) / HBM_PEAK_GBS, 4)},
             "rotation": rot,
+            "gathers": gathers,
             "chained": {"stage2_keys_mean": float(np.mean(ch.N + ch.R)),
                         "stage2_ms": round(ms2c, 4), "step_ms": round(ms1 + ms2c, 4),
                         "images_s": round(B / ((ms1 + ms2c) * 1e-3), 1),
@@ -1005,6 +1030,9 @@ def main():
             100 * rec["stages"]["stage1_score"]["hbm_frac"], rec["stages"]["stage2_ms"],
             100 * rec["stages"]["stage2_hbm_frac"], rec["stages"]["chained"]["step_ms"],
             rec["stages"]["chained"]["stage2_keys_mean"]))
+    g = rec["stages"]["gathers"]
+    log("gathers alone: Stage I %.1f us (a plain copy of the bytes %.1f us), Stage II %.1f us (%.1f us)" % (
+        g["stage1"]["gather_us"], g["stage1"]["copy_us"], g["stage2"]["gather_us"], g["stage2"]["copy_us"]))
     rec["ablation"] = ablation_steps(torch, dvs, dts, float(kept1.mean()), float(kept2.mean()),
                                      max(10, args.steps // 2))
     log("ablation: mean threshold %.3f ms/step, fixed budget %.3f ms/step" % (
