@@ -6,18 +6,21 @@
 // threshold    one thread per sample: tau = lambda * reduce(register scores); for
 //              the ablation's mean-based threshold one workgroup per sample
 //              averages the visual scores instead (sample_reference).
-// select       one workgroup per sample: every thread owns a contiguous strip
-//              of candidates, counts the strip's survivors, a wave scan plus a
-//              4-entry LDS scan gives each strip its output position, and the
-//              strip writes its survivors' candidate-local indices, ascending,
-//              to the sample's slot of the workspace (slot[co_b + i]).
-//              Optionally computes tau first (fused threshold of occam_prune).
+// select       one workgroup per sample: every wave owns a contiguous range of
+//              candidates and walks it 64 at a time, a ballot of the keep flags
+//              counting its survivors; an LDS scan of the wave totals places the
+//              ranges, and a second walk writes each survivor's candidate-local
+//              index, ascending, at its position (mbcnt below the lane) in the
+//              sample's slot of the workspace (slot[co_b + i]).  Optionally computes
+//              tau first (fused threshold of occam_prune).  The same compaction runs
+//              in the last workgroup of each sample of the Stage II scoring kernel.
 // pack_gather  grid (G, sample): every wave forms its sample's packed offset
 //              (exclusive sum of the counts before it, with shuffles: no
-//              barrier); the workgroups write the packed survivor list (through
-//              index_map when given) and kept_offsets, and their waves copy
-//              survivor rows of every row tensor with 16-byte vector loads and
-//              stores, one row per wave at a time.
+//              barrier); with Stage I's per-chunk lists, an LDS scan of the chunk
+//              counts concatenates them.  The workgroups write the packed survivor
+//              list (through index_map when given) and kept_offsets, and their
+//              waves copy survivor rows of every row tensor with 16-byte
+//              non-temporal loads and stores, one row per wave at a time.
 #include "occam_internal.hpp"
 
 namespace occam {
