@@ -145,3 +145,13 @@ def test_step_description_covers_ragged_workloads():
     assert bench.step_desc("llava_next", v, t) == (
         "llava_next: B=2, R=4, N=2880 visual tokens; Stage I CLS row H=16 d=64 + 1024-wide hidden "
         "gather; Stage II 128 text rows H=32 d=128 over all 2880 tokens + hidden/K/V gather")
+
+
+def test_cycler_runs_the_copies_in_turn():
+    # Every timed loop of the bench calls one cycled function per step: copy 0, 1, 2, 0, ...
+    seen = []
+    one = bench.cycler([lambda i=i: seen.append(i) for i in range(bench.NCOPY)])
+    for _ in range(2 * bench.NCOPY + 1):
+        one()
+    assert seen == list(range(bench.NCOPY)) * 2 + [0]
+    assert bench.NCOPY >= 3
