@@ -779,8 +779,8 @@ def main():
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: every sample is pruned independently, so a batch "
-              "shards across GPUs with no exchange and this build runs and measures one; "
-              "run it with --gpus 1", file=sys.stderr)
+              "shards across GPUs with no exchange, and the figure per GPU is the one-GPU "
+              "figure; run it with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -89,7 +89,7 @@ extern "C" {
 typedef enum {
     OCCAM_OK = 0,
     OCCAM_ERR_INVALID_ARG = 1, /* a null/misaligned pointer or an impossible shape   */
-    OCCAM_ERR_UNSUPPORTED = 2, /* a valid shape this build has no kernel for         */
+    OCCAM_ERR_UNSUPPORTED = 2, /* a valid shape the library has no kernel for        */
     OCCAM_ERR_WORKSPACE = 3,   /* ws_bytes < occam_workspace_size(problem)          */
     OCCAM_ERR_HIP = 4          /* a kernel launch was rejected by the HIP runtime    */
 } occam_status;
