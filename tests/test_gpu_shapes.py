@@ -59,3 +59,43 @@ def test_random_shape(case):
     check_scores(g["tau"], o["tau"], rtol, "tau")
     check_selection(g, o, sb, rtol)
     check_rows(g, sb)
+
+
+@pytest.mark.parametrize("case", _cases()[:24], ids=lambda c: "case%d" % c[0])
+def test_random_shape_unfused_equals_fused(case):
+    # occam_score, occam_threshold, occam_select and occam_gather in turn give the fused
+    # prune's scores, tau, survivors and rows bit for bit (the fused kernels run the same
+    # arithmetic in the same order).
+    import torch
+    from paper_2605_29657_amd import occam
+    i, form, dtype, B, R, H, Hkv, d, T, N, lam = case
+    print("case%d: %s dtype=%s B=%d R=%d H=%d Hkv=%d d=%d T=%s N=%s lam=%g" % (
+        i, form, dtype, B, R, H, Hkv, d, T, N, lam), flush=True)
+    sb = custom_stage(B=B, R=R, H=H, Hkv=Hkv, d=d, T=T, N=N, dtype=dtype, seed=1000 + i,
+                      stage=form)
+    ds = DeviceStage(sb, ragged=True)
+    ds.prune(lam)
+    fused = ds.host()
+    p, dev = ds.problem, "cuda"
+    scores = torch.empty(ds.total_keys, dtype=torch.float32, device=dev)
+    tau = torch.empty(sb.B, dtype=torch.float32, device=dev)
+    kept = torch.empty(max(ds.total_cands, 1), dtype=torch.int32, device=dev)
+    cnt = torch.empty(sb.B, dtype=torch.int32, device=dev)
+    offs = torch.empty(sb.B + 1, dtype=torch.int32, device=dev)
+    occam.score(p, ds.q, ds.k, scores, ds.ws)
+    occam.threshold(p, scores, lam, occam.REG_MEAN, tau)
+    occam.select(p, scores, tau, kept, cnt, offs, ds.ws)
+    dsts = [torch.zeros_like(x) for x in ds.row_dst]
+    rows = [occam.Rows(s, x, src_pad_rows=pl.pad_rows, src_row0=pl.row0)
+            for s, x, pl in zip(ds.row_src, dsts, sb.payload)]
+    occam.gather(p, rows, kept, offs)
+    torch.cuda.synchronize()
+    total = int(offs[-1])
+    assert np.array_equal(scores.cpu().numpy(), fused["scores"])
+    assert np.array_equal(tau.cpu().numpy(), fused["tau"])
+    assert np.array_equal(kept[:total].cpu().numpy(), fused["kept_idx"])
+    assert np.array_equal(offs.cpu().numpy(), fused["kept_offsets"])
+    for x, want in zip(dsts, fused["rows"]):
+        got = x[:total].cpu()
+        got = got.view(torch.int16).numpy().view(np.uint16) if got.dtype == torch.bfloat16 else got.numpy()
+        assert np.array_equal(got.view(np.uint8), want.view(np.uint8))
