@@ -777,25 +777,48 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
     if (!last_of_sample(fin.done, b, ntask, reinterpret_cast<int*>(smem_raw + 64))) return;
     if (part) {
         // Row maxima (visual keys) / row sums (registers) over the row blocks in order,
-        // then the head (and row) mean.
+        // then the head (and row) mean: text_rows_combine's arithmetic.  Each thread takes
+        // U keys at a time, so that U coherent loads per row block are in flight (one at a
+        // time cost ~70 us on a 16384-key sample).  With the threshold to follow, the
+        // scores also go straight into the LDS copy that it reads.
+        constexpr int U = 16;
         const size_t smax = (size_t)(p.R + p.max_cands);
         const float* pb = part + (size_t)b * nrb * smax;
         float* out = scores + k_begin(p, b);
-        for (int s = threadIdx.x; s < S; s += kScoreThreads) {
-            float v = 0.f;
-            if (s < p.R) {
-                for (int r = 0; r < nrb_b; ++r) v += ld<true>(pb + (size_t)r * smax + s);
-                v *= 1.f / ((float)p.H * (float)T);
-            } else {
-                for (int r = 0; r < nrb_b; ++r) v = fmaxf(v, ld<true>(pb + (size_t)r * smax + s));
-                v *= 1.f / (float)p.H;
+        float* sl = fin.select ? select_scores_lds(smem_raw + 128) : nullptr;
+        const float inv_reg = 1.f / ((float)p.H * (float)T), inv_vis = 1.f / (float)p.H;
+        for (int s0 = threadIdx.x; s0 < S; s0 += U * kScoreThreads) {
+            float v[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) v[u] = 0.f;
+            for (int r = 0; r < nrb_b; ++r) {
+                float x[U];
+#pragma unroll
+                for (int u = 0; u < U; ++u) {
+                    const int s = s0 + u * kScoreThreads;
+                    x[u] = s < S ? ld<true>(pb + (size_t)r * smax + s) : 0.f;
+                }
+#pragma unroll
+                for (int u = 0; u < U; ++u)
+                    v[u] = s0 + u * kScoreThreads < p.R ? v[u] + x[u] : fmaxf(v[u], x[u]);
             }
-            st_cc(out + s, v);          // read back below with coherent loads
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int s = s0 + u * kScoreThreads;
+                if (s < S) {
+                    const float w = v[u] * (s < p.R ? inv_reg : inv_vis);
+                    st_cc(out + s, w);
+                    if (sl) sl[s] = w;
+                }
+            }
         }
-        __builtin_amdgcn_s_waitcnt(0x0F70);
-        __syncthreads();
+        if (fin.select) {
+            __syncthreads();
+            select_sample(p, scores, b, fin, smem_raw + 128, true);
+        }
+        return;
     }
-    if (fin.select) select_sample(p, scores, b, fin, smem_raw + 128);
+    if (fin.select) select_sample(p, scores, b, fin, smem_raw + 128, false);
 }
 
 // Scores from the row blocks' partials: the maximum over row blocks (visual keys) or

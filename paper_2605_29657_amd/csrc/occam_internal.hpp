@@ -379,21 +379,27 @@ inline size_t select_lds_bytes(int R, int max_cands) {
     return kSelectScratch + 4 * ((size_t)R + (size_t)max_cands);
 }
 
+// Where select_sample keeps its copy of the sample's scores (lds as passed to it).
+__device__ __forceinline__ float* select_scores_lds(char* lds) {
+    return reinterpret_cast<float*>(lds + kSelectScratch);
+}
+
 // Threshold (tau_b = lambda * reference, the fused threshold of select_kernel) and
 // compaction of sample b by one workgroup of kSelThreads threads.  The sample's scores,
 // written by other workgroups of the launch, are first copied into LDS with
-// device-coherent loads (eight in flight per thread); the reference and the compaction
-// then read the copy, with select_kernel's arithmetic.  lds: select_lds_bytes(R, N_b).
+// device-coherent loads (eight in flight per thread), unless the caller has already put
+// them there (in_lds, followed by a barrier); the reference and the compaction then read
+// the copy, with select_kernel's arithmetic.  lds: select_lds_bytes(R, N_b).
 __device__ __forceinline__ void select_sample(const Prob& p, const float* scores, int b,
-                                              const Finish& f, char* lds) {
+                                              const Finish& f, char* lds, bool in_lds) {
     float* red = reinterpret_cast<float*>(lds);              // kSelThreads / 64 floats
     int* wsum = reinterpret_cast<int*>(lds + 16);            // kSelThreads / 64 ints
     float* tau_s = reinterpret_cast<float*>(lds + 32);
-    float* sl = reinterpret_cast<float*>(lds + kSelectScratch);
+    float* sl = select_scores_lds(lds);
     const int S = keys_of(p, b);
     const float* src = scores + k_begin(p, b);
     constexpr int U = 8;
-    for (int i0 = threadIdx.x; i0 < S; i0 += U * kSelThreads) {
+    for (int i0 = threadIdx.x; i0 < S && !in_lds; i0 += U * kSelThreads) {
         float v[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
