@@ -451,17 +451,26 @@ __global__ __launch_bounds__(kClsThreads) void cls_scores_kernel(
         }
     } else {
         // Merge the per-chunk (max, sum) pairs of the sample: P threads per head, each a
-        // strided subset of chunks, then a fixed-order merge of the P partials.
+        // strided subset of chunks (loaded PF at a time, so that long samples do not wait
+        // for one load after another), then a fixed-order merge of the P partials.
+        constexpr int PF = 8;
         const int P = blockDim.x / H;
         const int hh = threadIdx.x % H, j0 = threadIdx.x / H;
         float m = -INFINITY, z = 0.f;
         if (j0 < P) {
             const float2* st = stats + (size_t)b * nchunks * H + hh;
-            for (int j = j0; j < nch; j += P) {
-                const float2 v = st[(size_t)j * H];
-                const float mn = fmaxf(m, v.x);
-                z = z * cls_exp<BF16>(m - mn) + v.y * cls_exp<BF16>(v.x - mn);
-                m = mn;
+            for (int j = j0; j < nch; j += PF * P) {
+                float2 v[PF];
+#pragma unroll
+                for (int u = 0; u < PF; ++u)
+                    v[u] = j + u * P < nch ? st[(size_t)(j + u * P) * H] : make_float2(0.f, 0.f);
+#pragma unroll
+                for (int u = 0; u < PF; ++u) {
+                    if (j + u * P >= nch) break;
+                    const float mn = fmaxf(m, v[u].x);
+                    z = z * cls_exp<BF16>(m - mn) + v[u].y * cls_exp<BF16>(v[u].x - mn);
+                    m = mn;
+                }
             }
         }
         red_m[threadIdx.x] = m;
