@@ -749,6 +749,9 @@ def main():
                     help="skip the LLaVA-1.5, Qwen3-VL and video steps")
     ap.add_argument("--mutual-only", action="store_true",
                     help="run and print only the mutual-scoring Stage I measurement")
+    ap.add_argument("--step-only", action="store_true",
+                    help="time only the step of --workload and print a short JSON line (for a "
+                         "kernel trace whose statistics cover the step's kernels alone)")
     ap.add_argument("--kernel-reps", type=int, default=20,
                     help="timed repetitions of the dominant kernel alone")
     ap.add_argument("--kernel-only", action="store_true",
@@ -868,6 +871,14 @@ def main():
     ms = e0.elapsed_time(e1) / args.steps
     log("timed %d steps: %.3f ms/step (wall %.3f ms/step)" % (args.steps, ms,
                                                               wall * 1e3 / args.steps))
+    if args.step_only:
+        nbytes = stage_bytes(vis, kept1)["total"] + stage_bytes(txt, kept2)["total"]
+        print(json.dumps({"workload": step_desc(name, vis, txt), "steps": args.steps,
+                          "settle_steps": settle_steps, "ms_per_step": round(ms, 4),
+                          "images_s": round(B / (ms * 1e-3), 1),
+                          "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)}),
+              flush=True)
+        return
 
     b1 = stage_bytes(vis, kept1)
     b2 = stage_bytes(txt, kept2)
