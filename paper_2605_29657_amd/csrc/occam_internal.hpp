@@ -130,8 +130,18 @@ __device__ __forceinline__ float reference_of(const float* s, int R, int N, int 
     const float* sv = s + R;
     const bool part = threadIdx.x < NT;
     float acc = 0.f;
-    if (part)
-        for (int v = threadIdx.x; v < N; v += NT) acc += ld<CC>(sv + v);
+    if (part) {
+        // Eight loads in flight per thread; the sum still runs over v in order.
+        constexpr int U = 8;
+        for (int v0 = threadIdx.x; v0 < N; v0 += U * NT) {
+            float x[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) x[u] = v0 + u * NT < N ? ld<CC>(sv + v0 + u * NT) : 0.f;
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                if (v0 + u * NT < N) acc += x[u];
+        }
+    }
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
     __syncthreads();                          // `red` may still be read by a previous call
@@ -164,9 +174,21 @@ __device__ __forceinline__ void compact_of(const float* sv, int N, float tau, in
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int Q = (((N + NW - 1) / NW) + kWave - 1) & ~(kWave - 1);
     const int v0 = min(N, wave * Q), v1 = min(N, v0 + Q);
+    // Both walks load U groups of 64 candidates before testing them, so that U loads are in
+    // flight per lane (the scores may sit in global memory); the groups are taken in order.
+    constexpr int U = 8;
     int cnt = 0;
-    for (int v = v0 + lane; v - lane < v1; v += kWave)
-        cnt += __popcll(__ballot(v < v1 && sv[v] >= tau));
+    for (int vb = v0; vb < v1; vb += U * kWave) {
+        float x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int v = vb + u * kWave + lane;
+            x[u] = v < v1 ? sv[v] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            cnt += __popcll(__ballot(vb + u * kWave + lane < v1 && x[u] >= tau));
+    }
     __syncthreads();                          // `wsum` may still be read by a previous call
     if (lane == 0) wsum[wave] = cnt;
     __syncthreads();
@@ -176,13 +198,23 @@ __device__ __forceinline__ void compact_of(const float* sv, int N, float tau, in
         base += w < wave ? wsum[w] : 0;
         total += wsum[w];
     }
-    for (int v = v0 + lane; v - lane < v1; v += kWave) {
-        const bool keep = v < v1 && sv[v] >= tau;
-        const unsigned long long m = __ballot(keep);
-        const int below = (int)__builtin_amdgcn_mbcnt_hi((unsigned)(m >> 32),
-                                                         __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
-        if (keep) out[base + below] = v;
-        base += __popcll(m);
+    for (int vb = v0; vb < v1; vb += U * kWave) {
+        float x[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int v = vb + u * kWave + lane;
+            x[u] = v < v1 ? sv[v] : 0.f;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int v = vb + u * kWave + lane;
+            const bool keep = v < v1 && x[u] >= tau;
+            const unsigned long long m = __ballot(keep);
+            const int below = (int)__builtin_amdgcn_mbcnt_hi(
+                (unsigned)(m >> 32), __builtin_amdgcn_mbcnt_lo((unsigned)m, 0u));
+            if (keep) out[base + below] = v;
+            base += __popcll(m);
+        }
     }
     if (threadIdx.x == 0) *count = total;
 }
