@@ -779,8 +779,8 @@ __global__ __launch_bounds__(kScoreThreads, 2) void text_score_kernel(
         // Row maxima (visual keys) / row sums (registers) over the row blocks in order,
         // then the head (and row) mean: text_rows_combine's arithmetic.  Each thread takes
         // U keys at a time, so that U coherent loads per row block are in flight (one at a
-        // time cost ~70 us on a 16384-key sample).  With the threshold to follow, the
-        // scores also go straight into the LDS copy that it reads.
+        // time cost ~40 us on the video batch's 16384-key samples).  With the threshold to
+        // follow, the scores also go straight into the LDS copy that it reads.
         constexpr int U = 16;
         const size_t smax = (size_t)(p.R + p.max_cands);
         const float* pb = part + (size_t)b * nrb * smax;
